@@ -1,0 +1,182 @@
+"""Benchmark: feature-extraction images/sec to the split layer on one MI355X.
+
+Default workload: ResNet-50 (Bottleneck [3, 4, 6, 3]), inference batch-norm
+folded, bf16 weights and activations with fp32 accumulation, batch 256 of
+synthetic 3x224x224 images, split after layer4 (2048x7x7, layer 18).  One step
+is one ``hapi_extract`` call over the whole batch: every layer from the input
+to the split, plus writing the split activations in NCHW.  Weights are packed
+once beforehand (model reuse); images and weights are resident in HBM.
+
+Prints ONE JSON line with the throughput, the MFMA utilisation of the
+convolution kernels, a roofline entry for the dominant kernel family (timed
+with HIP events on the library's stream) and the CPU oracle timed on a bounded
+sample as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+PEAK = {"bf16": 2500.0, "f32": 157.3}  # dense MFMA TFLOP/s (MI355X)
+HBM_PEAK = 8000.0                      # GB/s
+
+
+def _cores():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS")
+    return min(n, int(omp)) if omp and omp.isdigit() else n
+
+
+def cpu_baseline(cfg, budget_s=15.0):
+    """The oracle on a bounded sample of the same workload (images/sec)."""
+    import synth
+    from oracle import layers as OL
+    from oracle import models as OM
+    threads = _cores()
+    OL.set_threads(threads)
+    om = OM.build(cfg["model"])
+    ps = synth.params(cfg["seed"], om.manifest())
+    imgs = synth.images(cfg["seed"], min(cfg["batch"], 64))
+    if cfg["dtype_name"] == "bf16":  # the oracle sees the bf16 values the GPU consumes
+        import torch
+        imgs = torch.from_numpy(imgs).to(torch.bfloat16).float().numpy()
+    t0 = time.perf_counter()
+    om.forward(ps, imgs[:1], cfg["split"])
+    t1 = time.perf_counter() - t0
+    n = int(max(1, min(len(imgs) - 1, budget_s / max(t1, 1e-3))))
+    t0 = time.perf_counter()
+    om.forward(ps, imgs[1:1 + n], cfg["split"])
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 4), "unit": "images/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} images of the same workload (images 1..{n}), float64 oracle, "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet50_bf16_b256")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload batch")
+    ap.add_argument("--chunk", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="time the library's plain copy (split 0) instead, for counter calibration")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the extraction shards "
+              "by images across GPUs with no communication, see the design notes.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2210_08650_amd as H
+    from paper_2210_08650_amd import models as PM
+    import synth
+
+    cfg = dict(PM.WORKLOADS[args.workload])
+    if args.batch:
+        cfg["batch"] = args.batch
+    cfg["dtype_name"] = "bf16" if cfg["dtype"] == H.HAPI_BF16 else "f32"
+    split = 0 if args.calib_copy else cfg["split"]
+    layers = PM.FACTORIES[cfg["model"]]()
+    B = cfg["batch"]
+    stream = torch.cuda.current_stream()
+    desc = H.Desc(layers, cfg["dtype"], stream=stream, chunk=args.chunk)
+    tdt = torch.bfloat16 if cfg["dtype"] == H.HAPI_BF16 else torch.float32
+
+    raw = torch.from_numpy(synth.flatten(synth.params(cfg["seed"], PM.raw_manifest(layers)))).cuda()
+    packed = torch.empty(H.hapi_packed_weight_bytes(desc), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    H.hapi_pack_weights(desc, raw, packed)
+    torch.cuda.synchronize()
+    load_ms = (time.perf_counter() - t0) * 1e3
+    del raw
+    images = torch.from_numpy(synth.images(cfg["seed"], B)).to(tdt).cuda()
+    out = torch.empty((B,) + H.hapi_layer_shape(desc, split), dtype=tdt, device="cuda")
+    ws_bytes = H.hapi_workspace_bytes(desc, B, split)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    desc.set(workspace=ws, workspace_bytes=ws_bytes)
+
+    def step():
+        H.hapi_extract(desc, packed, images, B, split, out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    # Per-kernel timing: HIP events around every launch, on the library's stream.
+    H.hapi_stats_enable(True)
+    t1 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    stats_elapsed = time.perf_counter() - t1
+    stats = H.hapi_stats_collect()
+    H.hapi_stats_enable(False)
+    fam = {s["name"]: s for s in stats}
+    conv_name = "conv_bf16" if cfg["dtype"] == H.HAPI_BF16 else "conv_f32"
+    total_kernel_ms = sum(s["total_ms"] for s in stats)
+    if args.calib_copy:
+        c = fam["copy"]
+        dom, bound, unit = c, "hbm", "GB/s"
+        achieved = c["bytes"] / (c["total_ms"] * 1e-3) / 1e9
+        peak = HBM_PEAK
+    else:
+        dom = fam[conv_name]
+        bound, unit = "mfma", "TFLOP/s"
+        achieved = dom["flops"] / (dom["total_ms"] * 1e-3) / 1e12
+        peak = PEAK[cfg["dtype_name"]]
+    mfma_util = None if args.calib_copy else round(100.0 * achieved / peak, 2)
+
+    result = {
+        "metric": "feature-extraction images/sec to split layer (ResNet-50 bf16 b=256); MFMA util %",
+        "value": round(B * args.steps / elapsed, 2),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype_name"],
+        "data": "synthetic (seeded N(0,1) images, He-init weights with seeded BN statistics)",
+        "config": {"workload": args.workload + ("_copy_calibration" if args.calib_copy else ""),
+                   "batch": B, "split_layer": split, "image": "3x224x224",
+                   "chunk": args.chunk or "auto",
+                   "partitions": H.hapi_chunk_count(desc, B)},
+        "mfma_util_pct": mfma_util,
+        "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": dom["name"], "launches_per_step": dom["launches"] // args.steps,
+                     "avg_launch_us": round(dom["total_ms"] * 1e3 / dom["launches"], 2),
+                     "share_of_kernel_time": round(dom["total_ms"] / total_kernel_ms, 4)},
+        "kernel_families": {s["name"]: {"ms_per_step": round(s["total_ms"] / args.steps, 4),
+                                        "launches_per_step": s["launches"] // args.steps}
+                            for s in stats},
+        "stats_pass_ms_per_step": round(stats_elapsed * 1e3 / args.steps, 4),
+        "model_load_ms": round(load_ms, 3),
+    }
+    if not args.no_cpu_baseline and not args.calib_copy:
+        result["cpu_baseline"] = cpu_baseline(cfg)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,220 @@
+/*
+ * hapi.h -- C ABI of the MI355X split feature-extraction library (libhapi.so).
+ *
+ * The library runs the storage-side half of split transfer learning: the
+ * forward pass of a frozen CNN or ViT feature extractor from the input images
+ * up to a chosen split layer (paper: Design and Implementation, "Request
+ * flow" -- the server executes feature extraction up to the split index; and
+ * System implementation -- custom models that run the forward pass between
+ * arbitrary layers), plus the per-layer output-size and forward-time profile
+ * that split selection consumes (Design, "Profiling and modeling runtime" and
+ * Table 1: output sizes from a batch-1 pass scale linearly with the batch;
+ * the server-side forward pass is a profiled phase).
+ *
+ * Conventions shared by every entry point
+ *  - Every data pointer is a DEVICE pointer owned by the caller (allocate with
+ *    hipMalloc or as torch tensors).  The library never allocates or frees
+ *    device memory except a few hipEvents for timing.
+ *  - Return value: HAPI_OK (0) or a negative hapi_status.  The message of the
+ *    last failure on the calling thread is returned by hapi_last_error().
+ *    Every argument is validated before anything is launched, so a call that
+ *    fails validation has written nothing.
+ *  - hapi_extract and hapi_pack_weights are asynchronous on desc->stream
+ *    (HIP stream semantics; the caller synchronises).  hapi_profile_layers
+ *    with out_us != NULL is synchronous.
+ *  - Calls are reentrant given distinct streams and distinct workspaces
+ *    (the paper's server runs up to 4 requests concurrently, Evaluation,
+ *    Methodology).  Calls sharing a workspace must be ordered by the caller.
+ *  - Results are deterministic: the same inputs give bit-identical outputs for
+ *    every chunk size and across runs (frozen weights make extraction
+ *    deterministic, Design, "Main insights" item 3; storage-side batch
+ *    adaptation must not change results, Storage-side batch size adaptation).
+ *
+ * Layer numbering: layer k (1-based) is desc->layers[k-1].  A residual block or
+ * transformer encoder block is one layer and ReLU / inference batch-norm belong
+ * to their convolution (paper, Measurement study: a block counts as one layer
+ * and only block boundaries are split points).  Split k means "the output of
+ * layer k"; split 0 is the input itself (Algorithm 1 ranges the split over
+ * [0, freeze index]; split 0 sends the raw input).
+ */
+#ifndef HAPI_H
+#define HAPI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HAPI_OK = 0,
+  HAPI_E_INVAL = -1,       /* bad argument: null pointer, split out of range, bad shape */
+  HAPI_E_UNSUPPORTED = -2, /* a layer kind / dtype / shape combination not built */
+  HAPI_E_NOMEM = -3,       /* workspace smaller than hapi_workspace_bytes() requires */
+  HAPI_E_DEVICE = -4       /* a HIP call or kernel launch failed */
+} hapi_status;
+
+typedef enum { HAPI_F32 = 0, HAPI_BF16 = 1 } hapi_dtype;
+
+/* Layer kinds and the fields each one reads (others must be 0).
+ *
+ * HAPI_CONV        cin, cout, k, stride, pad, has_bias, has_bn, relu.
+ *                  y = [ReLU]( BN( W * x + b ) ), zero padding, floor-mode size.
+ * HAPI_MAXPOOL     k, stride, pad: window max, padding counts as -infinity.
+ * HAPI_AVGPOOL     k == 0: global mean over H x W (output C x 1 x 1);
+ *                  k > 0: k x k window mean with the given stride, no padding.
+ * HAPI_BASIC_BLOCK cin, cout, stride:  ReLU(bn2(conv2(ReLU(bn1(conv1(x))))) + sc(x)),
+ *                  conv1 3x3/stride, conv2 3x3/1, sc = bn(conv1x1/stride) when
+ *                  stride != 1 or cin != cout, else identity.
+ * HAPI_BOTTLENECK  cin, width, stride:  ReLU(c3(c2(c1(x))) + sc(x)) with
+ *                  c1 1x1 cin->width, c2 3x3/stride width->width, c3 1x1
+ *                  width->4*width, each with BN (ReLU after c1, c2); sc as above.
+ * HAPI_PATCH_EMBED cin, cout (= model width D), k (= patch size, also the stride):
+ *                  non-overlapping patch projection with bias, no activation.
+ * HAPI_TOKENS      cout (= D): [N, D, h, w] -> [N, 1 + h*w, D]; patch t = row*w + col
+ *                  becomes token 1 + t, a class token is token 0, and the
+ *                  position embedding is added to every token.
+ * HAPI_VIT_BLOCK   cout (= D), heads, mlp_dim: pre-norm encoder block
+ *                  x += out_proj(MHA(LN1(x))); x += fc2(GELU(fc1(LN2(x)))),
+ *                  layernorm eps 1e-6, exact-erf GELU, softmax(QK^T/sqrt(D/heads))V.
+ * HAPI_LAYERNORM   cout (= D): per-token layernorm with affine, eps 1e-6.
+ *
+ * Batch-norm is inference-mode with eps 1e-5. */
+typedef enum {
+  HAPI_CONV = 0,
+  HAPI_MAXPOOL = 1,
+  HAPI_AVGPOOL = 2,
+  HAPI_BASIC_BLOCK = 3,
+  HAPI_BOTTLENECK = 4,
+  HAPI_PATCH_EMBED = 5,
+  HAPI_TOKENS = 6,
+  HAPI_VIT_BLOCK = 7,
+  HAPI_LAYERNORM = 8
+} hapi_kind;
+
+typedef struct {
+  int32_t kind;                       /* hapi_kind */
+  int32_t cin, cout, width;           /* channels (width: bottleneck inner width) */
+  int32_t k, stride, pad;             /* window / kernel geometry */
+  int32_t relu, has_bias, has_bn;     /* HAPI_CONV options (0/1) */
+  int32_t heads, mlp_dim;             /* HAPI_VIT_BLOCK */
+  int32_t reserved[4];                /* must be 0 */
+} hapi_layer;
+
+typedef struct {
+  int32_t n_layers;                   /* >= 1 */
+  const hapi_layer *layers;           /* host array of n_layers entries */
+  int32_t dtype;                      /* hapi_dtype of images, activations and outputs */
+  int32_t in_c, in_h, in_w;           /* per-image input shape (NCHW) */
+  void *stream;                       /* hipStream_t; NULL = the null stream */
+  void *workspace;                    /* device scratch owned by the caller */
+  size_t workspace_bytes;
+  int32_t chunk;                      /* storage-side (COS) batch: images per sequential
+                                         partition; 0 = the library chooses */
+} hapi_model_desc;
+
+/* Raw (unpacked) weights: ONE flat float32 device buffer holding, layer by
+ * layer in order, the PyTorch-layout tensors below (nothing for pools):
+ *   CONV         weight [cout, cin, k, k]; bias [cout] if has_bias;
+ *                gamma, beta, running_mean, running_var [cout] each if has_bn
+ *   BASIC_BLOCK  conv1 weight, bn1 (4 x [cout]); conv2 weight, bn2;
+ *                shortcut weight [cout, cin, 1, 1], shortcut bn (only if present)
+ *   BOTTLENECK   conv1 weight [width, cin, 1, 1], bn1; conv2 weight
+ *                [width, width, 3, 3], bn2; conv3 weight [4w, width, 1, 1], bn3;
+ *                shortcut weight + bn (only if present)
+ *   PATCH_EMBED  weight [D, cin, k, k], bias [D]
+ *   TOKENS       class token [D], position embedding [T, D] (T = 1 + h*w)
+ *   VIT_BLOCK    ln1 gamma, beta [D]; in-proj weight [3D, D] (rows: query, key,
+ *                value), bias [3D]; out-proj weight [D, D], bias [D]; ln2 gamma,
+ *                beta [D]; fc1 weight [mlp, D], bias [mlp]; fc2 weight [D, mlp], bias [D]
+ *   LAYERNORM    gamma, beta [D]
+ * Returns the number of float32 values, or a negative hapi_status. */
+int64_t hapi_raw_weight_count(const hapi_model_desc *desc);
+
+/* Bytes of the packed-weight buffer hapi_pack_weights writes, or < 0 on error. */
+int64_t hapi_packed_weight_bytes(const hapi_model_desc *desc);
+
+/* Model load (the "read model to GPU" phase of Table 1): folds inference
+ * batch-norm into the preceding convolution in float32 (W' = W g/sqrt(v+eps),
+ * b' = beta + (b - mean) g/sqrt(v+eps)), reorders convolution weights for the
+ * kernels and casts them to desc->dtype.  raw_weights: device float32 buffer of
+ * hapi_raw_weight_count() values (layout above); packed: device buffer of
+ * hapi_packed_weight_bytes() bytes, 256-byte aligned.  Packed weights are
+ * reused by any number of hapi_extract calls (model reuse, Design, "Request
+ * flow").  Asynchronous on desc->stream; needs no workspace. */
+int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void *packed);
+
+/* Per-image output shape of layer `layer` (0 = input) in the caller layout:
+ * NCHW {C, H, W} for convolutional layers (ndim 3), {T, D} for token layers
+ * (ndim 2).  dims must hold 3 values.  Host only. */
+int hapi_layer_shape(const hapi_model_desc *desc, int32_t layer, int64_t *dims, int32_t *ndim);
+
+/* Workspace bytes hapi_extract(batch, split_layer) needs with desc->chunk
+ * (profile != 0: what hapi_profile_layers(batch, out_us != NULL) needs, which
+ * also holds synthetic weights and inputs).  At least the paper's memory
+ * estimate -- the largest input + output of any layer at the chunk batch
+ * (Design, "Memory usage estimation"; over-estimating is the safe side) --
+ * plus block-internal temporaries.  Returns bytes or a negative hapi_status. */
+int64_t hapi_workspace_bytes(const hapi_model_desc *desc, int32_t batch, int32_t split_layer,
+                             int32_t profile);
+
+/* Number of sequential partitions (storage-side batches) hapi_extract uses for
+ * `batch` images with desc->chunk (Storage-side batch size adaptation: a
+ * request is processed as sequential partitions of the storage-side batch;
+ * the last partition may be short).  Host only; < 0 on error. */
+int32_t hapi_chunk_count(const hapi_model_desc *desc, int32_t batch);
+
+/* The storage-side forward pass.
+ *   weights      packed weights from hapi_pack_weights (same desc)
+ *   images       [batch, in_c, in_h, in_w] NCHW in desc->dtype
+ *   batch        >= 1 images
+ *   split_layer  0..n_layers: layers 1..split_layer run; 0 copies the input
+ *   out          [batch, <hapi_layer_shape(split_layer)>] in desc->dtype,
+ *                NCHW for convolutional layers, [batch, T, D] for token
+ *                layers; row i always belongs to image i
+ * The batch runs as hapi_chunk_count() sequential partitions through the
+ * workspace.  Errors: HAPI_E_INVAL (null pointer, batch < 1, split out of
+ * range), HAPI_E_NOMEM (workspace too small), HAPI_E_UNSUPPORTED,
+ * HAPI_E_DEVICE (a launch failed).  Asynchronous on desc->stream. */
+int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *images,
+                 int32_t batch, int32_t split_layer, void *out);
+
+/* Per-layer profile for split selection (Table 1; Measurement study, Fig. 2a/2b).
+ *   out_bytes[k], k = 0..n_layers: bytes of the layer-k output at `batch`
+ *                 (k = 0: the input), closed form, no device access.
+ *   out_us[k]:    device time in microseconds of layer k at `batch` with
+ *                 desc->chunk, median of 20 timed passes after 5 warm-ups, on
+ *                 synthetic weights and inputs written into the workspace
+ *                 (out_us[0] = 0).  NULL skips timing; then the call touches
+ *                 no device and works without a GPU.
+ * Synchronous.  With out_us the workspace must hold
+ * hapi_workspace_bytes(desc, batch, n_layers, 1) bytes. */
+int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out_bytes,
+                        float *out_us);
+
+/* Per-kernel timing of later hapi_extract calls (for roofline reporting).
+ * hapi_stats_enable(1) clears the counters and brackets every kernel launch of
+ * hapi_extract with HIP events on desc->stream; hapi_stats_enable(0) stops.
+ * hapi_stats_collect synchronises the recorded events and fills up to
+ * `max_entries` rows, one per kernel family, returning the number of families
+ * (or < 0).  flops / bytes are the algorithmic counts of the recorded launches. */
+typedef struct {
+  char name[32];
+  int64_t launches;
+  double total_ms;
+  double flops;
+  double bytes;
+} hapi_kernel_stat;
+
+int hapi_stats_enable(int32_t enable);
+int hapi_stats_collect(hapi_kernel_stat *out, int32_t max_entries);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *hapi_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HAPI_H */

@@ -1,0 +1,792 @@
+// Host runtime of libhapi: descriptor validation and shape calculus, weight
+// layout and packing, the chunked (storage-side batch) executor, per-layer
+// profiling and per-kernel timing.  Entry points are declared in hapi.h.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <functional>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace hapi {
+namespace {
+
+// ------------------------------------------------------------------ errors
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                  \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(HAPI_E_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));       \
+  } while (0)
+
+// ------------------------------------------------------------------ model
+
+constexpr int64_t kAlign = 256;
+constexpr int64_t kIndexLimit = (int64_t)1 << 31;  // kernels index a partition with int32
+constexpr int kAutoChunk = 256;
+
+int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Act {  // per-image activation, stored NHWC (tokens: h = T, w = 1, c = D)
+  int c = 0, h = 0, w = 0;
+  bool tok = false;
+  int64_t elems() const { return (int64_t)c * h * w; }
+};
+
+struct ConvSpec {
+  int cin, cout, k, stride, pad;
+  bool bias, bn;
+  int K, Kp;
+  int64_t raw_w, raw_b, raw_bn;  // float offsets into the raw buffer (-1: absent)
+  int64_t pk_w, pk_b;            // byte offsets into the packed buffer
+};
+
+struct Extra {  // float32 parameter copied verbatim (tokens, layernorm)
+  int64_t raw, pk, n;
+};
+
+struct LayerPlan {
+  hapi_layer L;
+  Act in, out;
+  std::vector<ConvSpec> convs;
+  std::vector<Extra> extras;
+  bool has_sc = false;
+  int64_t tmp_elems = 0;  // largest per-image tensor the layer reads or writes
+};
+
+struct Model {
+  bool bf16 = true;
+  int esz = 2;
+  Act input;
+  std::vector<LayerPlan> layers;
+  int64_t raw_count = 0, packed_bytes = 0;
+  bool first_reads_nchw = false;
+};
+
+int conv_out(int x, int k, int s, int p) { return (x + 2 * p - k) / s + 1; }
+
+int analyze(const hapi_model_desc *d, Model &m) {
+  if (!d) return fail(HAPI_E_INVAL, "desc is NULL");
+  if (d->n_layers < 1 || !d->layers) return fail(HAPI_E_INVAL, "desc has no layers");
+  if (d->dtype != HAPI_F32 && d->dtype != HAPI_BF16)
+    return fail(HAPI_E_INVAL, "unknown dtype %d", d->dtype);
+  if (d->in_c < 1 || d->in_h < 1 || d->in_w < 1)
+    return fail(HAPI_E_INVAL, "bad input shape %dx%dx%d", d->in_c, d->in_h, d->in_w);
+  if (d->chunk < 0) return fail(HAPI_E_INVAL, "chunk must be >= 0");
+  m = Model();
+  m.bf16 = d->dtype == HAPI_BF16;
+  m.esz = m.bf16 ? 2 : 4;
+  m.input = Act{d->in_c, d->in_h, d->in_w, false};
+  const int kq = m.bf16 ? 64 : 16;  // k-tile of the conv kernels
+  Act cur = m.input;
+  int64_t raw = 0, pk = 0;
+
+  auto add_conv = [&](LayerPlan &lp, int cin, int cout, int k, int s, int p, bool bias, bool bn) {
+    ConvSpec c{};
+    c.cin = cin; c.cout = cout; c.k = k; c.stride = s; c.pad = p; c.bias = bias; c.bn = bn;
+    c.K = cin * k * k;
+    c.Kp = (c.K + kq - 1) / kq * kq;
+    c.raw_w = raw; raw += (int64_t)cout * c.K;
+    c.raw_b = -1; c.raw_bn = -1;
+    if (bias) { c.raw_b = raw; raw += cout; }
+    if (bn) { c.raw_bn = raw; raw += 4 * (int64_t)cout; }
+    c.pk_w = pk; pk = align_up(pk + (int64_t)cout * c.Kp * m.esz);
+    c.pk_b = pk; pk = align_up(pk + (int64_t)cout * 4);
+    lp.convs.push_back(c);
+  };
+  auto add_extra = [&](LayerPlan &lp, int64_t n) {
+    lp.extras.push_back(Extra{raw, pk, n});
+    raw += n;
+    pk = align_up(pk + n * 4);
+  };
+  // NHWC-input convolutions need whole 16-byte chunks of channels per k-tile.
+  auto nhwc_ok = [&](int cin) { return cin % kq == 0; };
+
+  for (int li = 0; li < d->n_layers; ++li) {
+    const hapi_layer &L = d->layers[li];
+    LayerPlan lp;
+    lp.L = L;
+    lp.in = cur;
+    for (int r = 0; r < 4; ++r)
+      if (L.reserved[r]) return fail(HAPI_E_INVAL, "layer %d: reserved fields must be 0", li + 1);
+    const bool first = li == 0;
+    switch (L.kind) {
+      case HAPI_CONV: {
+        if (cur.tok) return fail(HAPI_E_INVAL, "layer %d: CONV on token input", li + 1);
+        if (L.cin != cur.c) return fail(HAPI_E_INVAL, "layer %d: cin %d != input channels %d", li + 1, L.cin, cur.c);
+        if (L.cout < 1 || L.k < 1 || L.stride < 1 || L.pad < 0 || L.pad >= L.k)
+          return fail(HAPI_E_INVAL, "layer %d: bad conv geometry", li + 1);
+        const int ho = conv_out(cur.h, L.k, L.stride, L.pad), wo = conv_out(cur.w, L.k, L.stride, L.pad);
+        if (ho < 1 || wo < 1) return fail(HAPI_E_INVAL, "layer %d: empty conv output", li + 1);
+        if (!first && !nhwc_ok(L.cin))
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: conv with cin %% %d != 0 after the first layer", li + 1, kq);
+        add_conv(lp, L.cin, L.cout, L.k, L.stride, L.pad, L.has_bias != 0, L.has_bn != 0);
+        lp.out = Act{L.cout, ho, wo, false};
+        if (first) m.first_reads_nchw = true;
+        break;
+      }
+      case HAPI_MAXPOOL:
+      case HAPI_AVGPOOL: {
+        if (cur.tok) return fail(HAPI_E_INVAL, "layer %d: pooling on token input", li + 1);
+        if (L.kind == HAPI_AVGPOOL && L.k == 0) {
+          lp.out = Act{cur.c, 1, 1, false};
+          break;
+        }
+        if (L.k < 1 || L.stride < 1 || L.pad < 0 || 2 * L.pad > L.k)
+          return fail(HAPI_E_INVAL, "layer %d: bad pooling geometry", li + 1);
+        if (L.kind == HAPI_AVGPOOL && L.pad != 0)
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: padded average pooling", li + 1);
+        if (L.kind == HAPI_MAXPOOL && cur.c % 8 != 0)
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: max pooling needs channels %% 8 == 0", li + 1);
+        const int ho = conv_out(cur.h, L.k, L.stride, L.pad), wo = conv_out(cur.w, L.k, L.stride, L.pad);
+        if (ho < 1 || wo < 1) return fail(HAPI_E_INVAL, "layer %d: empty pooling output", li + 1);
+        lp.out = Act{cur.c, ho, wo, false};
+        break;
+      }
+      case HAPI_BASIC_BLOCK:
+      case HAPI_BOTTLENECK: {
+        if (cur.tok) return fail(HAPI_E_INVAL, "layer %d: residual block on token input", li + 1);
+        if (L.cin != cur.c) return fail(HAPI_E_INVAL, "layer %d: cin %d != input channels %d", li + 1, L.cin, cur.c);
+        if (L.stride < 1) return fail(HAPI_E_INVAL, "layer %d: stride must be >= 1", li + 1);
+        const bool basic = L.kind == HAPI_BASIC_BLOCK;
+        const int width = basic ? L.cout : L.width;
+        const int cout = basic ? L.cout : 4 * L.width;
+        if (width < 1) return fail(HAPI_E_INVAL, "layer %d: bad block width", li + 1);
+        if (!basic && L.cout != 0 && L.cout != cout)
+          return fail(HAPI_E_INVAL, "layer %d: bottleneck cout must be 4 * width", li + 1);
+        if (!nhwc_ok(L.cin) || !nhwc_ok(width) || !nhwc_ok(cout))
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: block channels must be multiples of %d", li + 1, kq);
+        const int ho = conv_out(cur.h, 3, L.stride, 1), wo = conv_out(cur.w, 3, L.stride, 1);
+        if (ho < 1 || wo < 1) return fail(HAPI_E_INVAL, "layer %d: empty block output", li + 1);
+        lp.has_sc = L.stride != 1 || L.cin != cout;
+        if (basic) {
+          add_conv(lp, L.cin, cout, 3, L.stride, 1, false, true);
+          add_conv(lp, cout, cout, 3, 1, 1, false, true);
+        } else {
+          add_conv(lp, L.cin, width, 1, 1, 0, false, true);
+          add_conv(lp, width, width, 3, L.stride, 1, false, true);
+          add_conv(lp, width, cout, 1, 1, 0, false, true);
+        }
+        if (lp.has_sc) add_conv(lp, L.cin, cout, 1, L.stride, 0, false, true);
+        lp.out = Act{cout, ho, wo, false};
+        lp.tmp_elems = std::max<int64_t>(lp.tmp_elems, (int64_t)width * cur.h * cur.w);
+        lp.tmp_elems = std::max<int64_t>(lp.tmp_elems, (int64_t)width * ho * wo);
+        break;
+      }
+      case HAPI_PATCH_EMBED: {
+        if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: PATCH_EMBED needs bf16", li + 1);
+        if (cur.tok || L.cin != cur.c) return fail(HAPI_E_INVAL, "layer %d: bad PATCH_EMBED input", li + 1);
+        if (L.k < 1 || (L.stride != 0 && L.stride != L.k) || L.pad != 0 || L.cout < 1)
+          return fail(HAPI_E_INVAL, "layer %d: bad patch geometry", li + 1);
+        if (!first && !nhwc_ok(L.cin))
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: PATCH_EMBED after the first layer needs cin %% 64 == 0", li + 1);
+        const int ho = cur.h / L.k, wo = cur.w / L.k;
+        if (ho < 1 || wo < 1) return fail(HAPI_E_INVAL, "layer %d: image smaller than a patch", li + 1);
+        add_conv(lp, L.cin, L.cout, L.k, L.k, 0, true, false);
+        lp.out = Act{L.cout, ho, wo, false};
+        if (first) m.first_reads_nchw = true;
+        break;
+      }
+      case HAPI_TOKENS: {
+        if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: TOKENS needs bf16", li + 1);
+        if (cur.tok || L.cout != cur.c) return fail(HAPI_E_INVAL, "layer %d: TOKENS width mismatch", li + 1);
+        if (L.cout % 8 != 0) return fail(HAPI_E_UNSUPPORTED, "layer %d: TOKENS width %% 8 != 0", li + 1);
+        const int T = 1 + cur.h * cur.w;
+        add_extra(lp, L.cout);
+        add_extra(lp, (int64_t)T * L.cout);
+        lp.out = Act{L.cout, T, 1, true};
+        break;
+      }
+      case HAPI_VIT_BLOCK: {
+        if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: VIT_BLOCK needs bf16", li + 1);
+        const int D = L.cout;
+        if (!cur.tok || D != cur.c) return fail(HAPI_E_INVAL, "layer %d: VIT_BLOCK input mismatch", li + 1);
+        if (L.heads < 1 || D % L.heads != 0 || L.mlp_dim < 1)
+          return fail(HAPI_E_INVAL, "layer %d: bad heads / mlp_dim", li + 1);
+        if (D / L.heads != kHeadDim)
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: head dim %d (only %d built)", li + 1, D / L.heads, kHeadDim);
+        if (D % 64 != 0 || L.mlp_dim % 64 != 0)
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: width and mlp_dim must be multiples of 64", li + 1);
+        if (cur.h > kAttnMaxTokens)
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: %d tokens (at most %d)", li + 1, cur.h, kAttnMaxTokens);
+        add_extra(lp, D);  // ln1 gamma
+        add_extra(lp, D);  // ln1 beta
+        add_conv(lp, D, 3 * D, 1, 1, 0, true, false);  // in-projection
+        add_conv(lp, D, D, 1, 1, 0, true, false);      // out-projection
+        add_extra(lp, D);  // ln2 gamma
+        add_extra(lp, D);  // ln2 beta
+        add_conv(lp, D, L.mlp_dim, 1, 1, 0, true, false);  // fc1
+        add_conv(lp, L.mlp_dim, D, 1, 1, 0, true, false);  // fc2
+        lp.out = cur;
+        lp.tmp_elems = (int64_t)cur.h * std::max(3 * D, L.mlp_dim);
+        break;
+      }
+      case HAPI_LAYERNORM: {
+        if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: LAYERNORM needs bf16", li + 1);
+        if (!cur.tok || L.cout != cur.c) return fail(HAPI_E_INVAL, "layer %d: LAYERNORM input mismatch", li + 1);
+        if (L.cout % 8 != 0 || L.cout > 2048)
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: LAYERNORM width must be a multiple of 8, <= 2048", li + 1);
+        add_extra(lp, L.cout);
+        add_extra(lp, L.cout);
+        lp.out = cur;
+        break;
+      }
+      default:
+        return fail(HAPI_E_INVAL, "layer %d: unknown kind %d", li + 1, L.kind);
+    }
+    if (first && !m.first_reads_nchw && m.input.c % 8 != 0 && L.kind == HAPI_MAXPOOL)
+      return fail(HAPI_E_UNSUPPORTED, "layer 1: max pooling needs channels %% 8 == 0");
+    lp.tmp_elems = std::max({lp.tmp_elems, lp.in.elems(), lp.out.elems()});
+    m.layers.push_back(lp);
+    cur = lp.out;
+  }
+  m.raw_count = raw;
+  m.packed_bytes = pk;
+  return HAPI_OK;
+}
+
+int64_t max_tmp(const Model &m, int split) {
+  int64_t t = m.first_reads_nchw ? 0 : m.input.elems();
+  for (int i = 0; i < split; ++i) t = std::max(t, m.layers[i].tmp_elems);
+  return t;
+}
+
+int chunk_for(const hapi_model_desc *d, const Model &m, int batch) {
+  int c = d->chunk > 0 ? std::min(d->chunk, batch) : std::min(batch, kAutoChunk);
+  if (d->chunk == 0) {
+    const int64_t per = std::max<int64_t>(1, max_tmp(m, (int)m.layers.size()));
+    const int64_t lim = (kIndexLimit - 1) / per;
+    c = (int)std::max<int64_t>(1, std::min<int64_t>(c, lim));
+  }
+  return c;
+}
+
+int64_t slot_bytes(const Model &m, int split, int chunk) {
+  return align_up((int64_t)chunk * max_tmp(m, split) * m.esz);
+}
+
+int64_t workspace_for(const Model &m, int split, int chunk, bool profile, int batch) {
+  int64_t b = split > 0 ? 3 * slot_bytes(m, split, chunk) : 0;
+  if (profile) b += align_up(m.packed_bytes) + align_up((int64_t)batch * m.input.elems() * m.esz);
+  return b;
+}
+
+// ------------------------------------------------------------- kernel stats
+
+enum Family { F_CONV_BF16, F_CONV_F32, F_ATTN, F_LN, F_MAXPOOL, F_AVGPOOL, F_TOKENS, F_LAYOUT,
+              F_COPY, F_COUNT };
+const char *kFamily[F_COUNT] = {"conv_bf16", "conv_f32", "attention", "layernorm", "maxpool",
+                                "avgpool", "tokens", "layout", "copy"};
+
+struct StatRec {
+  int fam;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+
+std::mutex g_stats_mu;
+bool g_stats_on = false;
+std::vector<StatRec> g_recs;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t take_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+hipError_t timed(hipStream_t s, int fam, double flops, double bytes, F &&launch) {
+  if (!g_stats_on) return launch();
+  std::lock_guard<std::mutex> g(g_stats_mu);
+  hipEvent_t a = take_event(), b = take_event();
+  if (a) (void)hipEventRecord(a, s);
+  hipError_t r = launch();
+  if (b) (void)hipEventRecord(b, s);
+  if (a && b) g_recs.push_back(StatRec{fam, a, b, flops, bytes});
+  return r;
+}
+
+// ------------------------------------------------------------------ executor
+
+struct Ctx {
+  const Model &m;
+  hipStream_t s;
+  const uint8_t *pk;
+  uint8_t *slot[3];
+  std::function<void(int, bool)> on_layer;  // (layer index, begin) for profiling
+};
+
+hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &in, int nb,
+                    void *y, const void *res, bool relu, bool gelu, bool nchw_input) {
+  ConvArgs a{};
+  a.x = x;
+  a.w = c.pk + cs.pk_w;
+  a.bias = reinterpret_cast<const float *>(c.pk + cs.pk_b);
+  a.res = res;
+  a.y = y;
+  a.n_img = nb;
+  a.H = in.h;
+  a.W = in.w;
+  a.C = in.c;
+  a.kh = a.kw = cs.k;
+  a.stride = cs.stride;
+  a.pad = cs.pad;
+  a.Ho = conv_out(in.h, cs.k, cs.stride, cs.pad);
+  a.Wo = conv_out(in.w, cs.k, cs.stride, cs.pad);
+  a.M = nb * a.Ho * a.Wo;
+  a.N = cs.cout;
+  a.K = cs.K;
+  a.Kp = cs.Kp;
+  a.ldc = cs.cout;
+  a.ldr = cs.cout;
+  a.relu = relu;
+  a.gelu = gelu;
+  Loader ld;
+  if (nchw_input) {
+    const bool vec_ok = c.m.bf16 && cs.k % 8 == 0 && cs.stride % 8 == 0 && cs.pad == 0 &&
+                        in.w % 8 == 0 && ((uintptr_t)x % 16) == 0;
+    ld = vec_ok ? LD_NCHW_PATCH : LD_NCHW;
+  } else {
+    ld = (cs.k == 1 && cs.stride == 1 && cs.pad == 0) ? LD_GEMM : LD_NHWC;
+  }
+  const double flops = 2.0 * a.M * (double)a.N * a.K;
+  const double bytes = (double)c.m.esz * ((double)nb * in.elems() + (double)a.M * a.N * (res ? 2 : 1) +
+                                          (double)a.N * a.K);
+  if (c.m.bf16)
+    return timed(c.s, F_CONV_BF16, flops, bytes, [&] { return launch_conv_bf16(a, ld, c.s); });
+  return timed(c.s, F_CONV_F32, flops, bytes, [&] { return launch_conv_f32(a, ld, c.s); });
+}
+
+// Runs layers 1..split on nb images; writes the split output (caller layout)
+// to `out` unless it is null (profiling).
+int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
+  const Model &m = c.m;
+  const bool bf = m.bf16;
+  const void *cur = images;
+  int cur_slot = -1;
+  auto free_slot = [&](int a = -1, int b = -1) {
+    for (int i = 0; i < 3; ++i)
+      if (i != cur_slot && i != a && i != b) return i;
+    return -1;
+  };
+  if (!m.first_reads_nchw) {
+    HIP_TRY(timed(c.s, F_LAYOUT, 0.0, 2.0 * nb * m.input.elems() * m.esz, [&] {
+      return launch_nchw_to_nhwc(bf, images, c.slot[0], nb, m.input.h * m.input.w, m.input.c, c.s);
+    }));
+    cur = c.slot[0];
+    cur_slot = 0;
+  }
+  for (int li = 0; li < split; ++li) {
+    const LayerPlan &lp = m.layers[li];
+    const hapi_layer &L = lp.L;
+    if (c.on_layer) c.on_layer(li, true);
+    const bool nchw_in = (li == 0) && m.first_reads_nchw;
+    switch (L.kind) {
+      case HAPI_CONV:
+      case HAPI_PATCH_EMBED: {
+        const int o = free_slot();
+        HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[o], nullptr,
+                         L.kind == HAPI_CONV && L.relu, false, nchw_in));
+        cur = c.slot[o];
+        cur_slot = o;
+        break;
+      }
+      case HAPI_MAXPOOL: {
+        const int o = free_slot();
+        HIP_TRY(timed(c.s, F_MAXPOOL, (double)nb * lp.out.elems() * L.k * L.k,
+                      (double)nb * (lp.in.elems() + lp.out.elems()) * m.esz, [&] {
+                        return launch_maxpool(bf, cur, c.slot[o], nb, lp.in.h, lp.in.w, lp.in.c, L.k,
+                                              L.stride, L.pad, lp.out.h, lp.out.w, c.s);
+                      }));
+        cur = c.slot[o];
+        cur_slot = o;
+        break;
+      }
+      case HAPI_AVGPOOL: {
+        const int o = free_slot();
+        HIP_TRY(timed(c.s, F_AVGPOOL, (double)nb * lp.in.elems(),
+                      (double)nb * (lp.in.elems() + lp.out.elems()) * m.esz, [&] {
+                        return launch_avgpool(bf, cur, c.slot[o], nb, lp.in.h, lp.in.w, lp.in.c, L.k,
+                                              L.stride, lp.out.h, lp.out.w, c.s);
+                      }));
+        cur = c.slot[o];
+        cur_slot = o;
+        break;
+      }
+      case HAPI_BASIC_BLOCK: {
+        const int A = free_slot();
+        const Act mid{lp.out.c, lp.out.h, lp.out.w, false};
+        HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
+        const void *res = cur;
+        if (lp.has_sc) {
+          const int B = free_slot(A);
+          HIP_TRY(run_conv(c, lp.convs[2], cur, lp.in, nb, c.slot[B], nullptr, false, false, false));
+          res = c.slot[B];
+        }
+        // In place over the block input: each output element's residual is read
+        // by the same thread right before that element is written.
+        HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], mid, nb, c.slot[cur_slot], res, true, false, false));
+        cur = c.slot[cur_slot];
+        break;
+      }
+      case HAPI_BOTTLENECK: {
+        const int A = free_slot(), B = free_slot(A);
+        const int width = L.width;
+        const Act a1{width, lp.in.h, lp.in.w, false};
+        const Act a2{width, lp.out.h, lp.out.w, false};
+        HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
+        HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], a1, nb, c.slot[B], nullptr, true, false, false));
+        const void *res = cur;
+        if (lp.has_sc) {
+          HIP_TRY(run_conv(c, lp.convs[3], cur, lp.in, nb, c.slot[A], nullptr, false, false, false));
+          res = c.slot[A];
+        }
+        HIP_TRY(run_conv(c, lp.convs[2], c.slot[B], a2, nb, c.slot[cur_slot], res, true, false, false));
+        cur = c.slot[cur_slot];
+        break;
+      }
+      case HAPI_TOKENS: {
+        const int o = free_slot();
+        const int T = lp.out.h, D = lp.out.c;
+        HIP_TRY(timed(c.s, F_TOKENS, (double)nb * T * D, 2.0 * nb * T * D * m.esz, [&] {
+          return launch_tokens(cur, reinterpret_cast<const float *>(c.pk + lp.extras[0].pk),
+                               reinterpret_cast<const float *>(c.pk + lp.extras[1].pk), c.slot[o], nb,
+                               T, D, c.s);
+        }));
+        cur = c.slot[o];
+        cur_slot = o;
+        break;
+      }
+      case HAPI_VIT_BLOCK: {
+        const int A = free_slot(), B = free_slot(A);
+        const int T = lp.in.h, D = lp.in.c;
+        const int64_t rows = (int64_t)nb * T;
+        // token matrices as NHWC images of one row: n = 1, H = rows, W = 1
+        const Act tokD{D, (int)rows, 1, false};
+        const Act tokF{L.mlp_dim, (int)rows, 1, false};
+        auto ln = [&](const Extra &g, const Extra &b, const void *x, void *y) {
+          return timed(c.s, F_LN, 8.0 * rows * D, 2.0 * rows * D * m.esz, [&] {
+            return launch_layernorm(x, reinterpret_cast<const float *>(c.pk + g.pk),
+                                    reinterpret_cast<const float *>(c.pk + b.pk), y, rows, D, 1e-6f, c.s);
+          });
+        };
+        HIP_TRY(ln(lp.extras[0], lp.extras[1], cur, c.slot[A]));
+        HIP_TRY(run_conv(c, lp.convs[0], c.slot[A], tokD, 1, c.slot[B], nullptr, false, false, false));
+        HIP_TRY(timed(c.s, F_ATTN, 4.0 * nb * (double)T * T * D, 4.0 * rows * D * m.esz, [&] {
+          return launch_attention(c.slot[B], c.slot[A], nb, T, D, L.heads, c.s);
+        }));
+        HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], tokD, 1, c.slot[cur_slot], cur, false, false, false));
+        HIP_TRY(ln(lp.extras[2], lp.extras[3], cur, c.slot[A]));
+        HIP_TRY(run_conv(c, lp.convs[2], c.slot[A], tokD, 1, c.slot[B], nullptr, false, true, false));
+        HIP_TRY(run_conv(c, lp.convs[3], c.slot[B], tokF, 1, c.slot[cur_slot], cur, false, false, false));
+        break;
+      }
+      case HAPI_LAYERNORM: {
+        const int o = free_slot();
+        const int64_t rows = (int64_t)nb * lp.in.h;
+        const int D = lp.in.c;
+        HIP_TRY(timed(c.s, F_LN, 8.0 * rows * D, 2.0 * rows * D * m.esz, [&] {
+          return launch_layernorm(cur, reinterpret_cast<const float *>(c.pk + lp.extras[0].pk),
+                                  reinterpret_cast<const float *>(c.pk + lp.extras[1].pk), c.slot[o],
+                                  rows, D, 1e-6f, c.s);
+        }));
+        cur = c.slot[o];
+        cur_slot = o;
+        break;
+      }
+      default:
+        return fail(HAPI_E_INVAL, "layer %d: unknown kind", li + 1);
+    }
+    if (c.on_layer) c.on_layer(li, false);
+  }
+  if (out) {
+    const Act &o = m.layers[split - 1].out;
+    const int64_t bytes = (int64_t)nb * o.elems() * m.esz;
+    if (o.tok || o.h * o.w == 1 || o.c == 1) {
+      HIP_TRY(timed(c.s, F_COPY, 0.0, 2.0 * bytes, [&] { return launch_copy(cur, out, bytes, c.s); }));
+    } else {
+      HIP_TRY(timed(c.s, F_LAYOUT, 0.0, 2.0 * bytes, [&] {
+        return launch_nhwc_to_nchw(bf, cur, out, nb, o.h * o.w, o.c, c.s);
+      }));
+    }
+  }
+  return HAPI_OK;
+}
+
+int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, const void *images,
+              int batch, int split, void *out, uint8_t *ws, int chunk,
+              const std::function<void(int, bool)> &on_layer) {
+  hipStream_t s = static_cast<hipStream_t>(d->stream);
+  const int64_t sb = slot_bytes(m, split, chunk);
+  Ctx c{m, s, static_cast<const uint8_t *>(weights), {ws, ws + sb, ws + 2 * sb}, on_layer};
+  const int64_t in_bytes = m.input.elems() * m.esz;
+  const int64_t out_bytes = m.layers[split - 1].out.elems() * m.esz;
+  for (int b0 = 0; b0 < batch; b0 += chunk) {
+    const int nb = std::min(chunk, batch - b0);
+    const int r = run_chunk(c, static_cast<const uint8_t *>(images) + (int64_t)b0 * in_bytes, nb, split,
+                            out ? static_cast<uint8_t *>(out) + (int64_t)b0 * out_bytes : nullptr);
+    if (r != HAPI_OK) return r;
+  }
+  return HAPI_OK;
+}
+
+}  // namespace
+}  // namespace hapi
+
+using namespace hapi;
+
+extern "C" {
+
+int64_t hapi_raw_weight_count(const hapi_model_desc *desc) {
+  Model m;
+  const int r = analyze(desc, m);
+  return r != HAPI_OK ? r : m.raw_count;
+}
+
+int64_t hapi_packed_weight_bytes(const hapi_model_desc *desc) {
+  Model m;
+  const int r = analyze(desc, m);
+  return r != HAPI_OK ? r : m.packed_bytes;
+}
+
+int hapi_layer_shape(const hapi_model_desc *desc, int32_t layer, int64_t *dims, int32_t *ndim) {
+  Model m;
+  const int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (!dims || !ndim) return fail(HAPI_E_INVAL, "dims / ndim is NULL");
+  if (layer < 0 || layer > (int)m.layers.size())
+    return fail(HAPI_E_INVAL, "layer %d outside [0, %d]", layer, (int)m.layers.size());
+  const Act a = layer == 0 ? m.input : m.layers[layer - 1].out;
+  if (a.tok) {
+    *ndim = 2; dims[0] = a.h; dims[1] = a.c; dims[2] = 0;
+  } else {
+    *ndim = 3; dims[0] = a.c; dims[1] = a.h; dims[2] = a.w;
+  }
+  return HAPI_OK;
+}
+
+int32_t hapi_chunk_count(const hapi_model_desc *desc, int32_t batch) {
+  Model m;
+  const int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (batch < 1) return fail(HAPI_E_INVAL, "batch must be >= 1");
+  const int c = chunk_for(desc, m, batch);
+  return (batch + c - 1) / c;
+}
+
+int64_t hapi_workspace_bytes(const hapi_model_desc *desc, int32_t batch, int32_t split_layer,
+                             int32_t profile) {
+  Model m;
+  const int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (batch < 1) return fail(HAPI_E_INVAL, "batch must be >= 1");
+  if (split_layer < 0 || split_layer > (int)m.layers.size())
+    return fail(HAPI_E_INVAL, "split %d outside [0, %d]", split_layer, (int)m.layers.size());
+  const int chunk = chunk_for(desc, m, batch);
+  if ((int64_t)chunk * max_tmp(m, split_layer) >= kIndexLimit)
+    return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
+  return workspace_for(m, split_layer, chunk, profile != 0, batch);
+}
+
+int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void *packed) {
+  Model m;
+  int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (m.packed_bytes == 0) return HAPI_OK;  // a model without parameters (pools only)
+  if (!raw_weights || !packed) return fail(HAPI_E_INVAL, "raw_weights / packed is NULL");
+  if ((uintptr_t)packed % kAlign) return fail(HAPI_E_INVAL, "packed must be 256-byte aligned");
+  if ((uintptr_t)raw_weights % 4) return fail(HAPI_E_INVAL, "raw_weights must be 4-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(desc->stream);
+  const float *raw = static_cast<const float *>(raw_weights);
+  uint8_t *pk = static_cast<uint8_t *>(packed);
+  for (size_t li = 0; li < m.layers.size(); ++li) {
+    const LayerPlan &lp = m.layers[li];
+    const bool nchw = li == 0 && m.first_reads_nchw;
+    for (const ConvSpec &c : lp.convs) {
+      const float *bn = c.raw_bn >= 0 ? raw + c.raw_bn : nullptr;
+      HIP_TRY(launch_pack_conv(m.bf16, raw + c.raw_w, c.raw_b >= 0 ? raw + c.raw_b : nullptr,
+                               bn, bn ? bn + c.cout : nullptr, bn ? bn + 2 * c.cout : nullptr,
+                               bn ? bn + 3 * c.cout : nullptr, c.cout, c.cin, c.k, c.k, c.Kp, nchw,
+                               pk + c.pk_w, reinterpret_cast<float *>(pk + c.pk_b), s));
+    }
+    for (const Extra &e : lp.extras)
+      HIP_TRY(launch_copy_f32(raw + e.raw, reinterpret_cast<float *>(pk + e.pk), e.n, s));
+  }
+  return HAPI_OK;
+}
+
+int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *images,
+                 int32_t batch, int32_t split_layer, void *out) {
+  Model m;
+  int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (!images || !out) return fail(HAPI_E_INVAL, "images / out is NULL");
+  if (batch < 1) return fail(HAPI_E_INVAL, "batch must be >= 1");
+  if (split_layer < 0 || split_layer > (int)m.layers.size())
+    return fail(HAPI_E_INVAL, "split %d outside [0, %d]", split_layer, (int)m.layers.size());
+  hipStream_t s = static_cast<hipStream_t>(desc->stream);
+  if (split_layer == 0) {  // no split: the raw input is the result
+    const int64_t bytes = (int64_t)batch * m.input.elems() * m.esz;
+    HIP_TRY(timed(s, F_COPY, 0.0, 2.0 * bytes, [&] { return launch_copy(images, out, bytes, s); }));
+    return HAPI_OK;
+  }
+  if (!weights && m.packed_bytes > 0) return fail(HAPI_E_INVAL, "weights is NULL");
+  if ((uintptr_t)weights % kAlign) return fail(HAPI_E_INVAL, "weights must be 256-byte aligned");
+  if ((uintptr_t)images % m.esz || (uintptr_t)out % m.esz)
+    return fail(HAPI_E_INVAL, "images / out are not aligned to the element size");
+  const int chunk = chunk_for(desc, m, batch);
+  if ((int64_t)chunk * max_tmp(m, split_layer) >= kIndexLimit)
+    return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
+  const int64_t need = workspace_for(m, split_layer, chunk, false, batch);
+  if (!desc->workspace || (int64_t)desc->workspace_bytes < need)
+    return fail(HAPI_E_NOMEM, "workspace of %zu bytes, %lld needed", desc->workspace_bytes,
+                (long long)need);
+  if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
+  return run_batch(desc, m, weights, images, batch, split_layer, out,
+                   static_cast<uint8_t *>(desc->workspace), chunk, nullptr);
+}
+
+int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out_bytes,
+                        float *out_us) {
+  Model m;
+  int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (batch < 1) return fail(HAPI_E_INVAL, "batch must be >= 1");
+  if (!out_bytes && !out_us) return fail(HAPI_E_INVAL, "out_bytes and out_us are both NULL");
+  const int n = (int)m.layers.size();
+  if (out_bytes) {
+    out_bytes[0] = (int64_t)batch * m.input.elems() * m.esz;
+    for (int k = 1; k <= n; ++k) out_bytes[k] = (int64_t)batch * m.layers[k - 1].out.elems() * m.esz;
+  }
+  if (!out_us) return HAPI_OK;
+
+  const int chunk = chunk_for(desc, m, batch);
+  if ((int64_t)chunk * max_tmp(m, n) >= kIndexLimit)
+    return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
+  const int64_t need = workspace_for(m, n, chunk, true, batch);
+  if (!desc->workspace || (int64_t)desc->workspace_bytes < need)
+    return fail(HAPI_E_NOMEM, "workspace of %zu bytes, %lld needed", desc->workspace_bytes,
+                (long long)need);
+  if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(desc->stream);
+  uint8_t *ws = static_cast<uint8_t *>(desc->workspace);
+  const int64_t slots = 3 * slot_bytes(m, n, chunk);
+  uint8_t *pk = ws + slots;
+  uint8_t *img = pk + align_up(m.packed_bytes);
+  // Synthetic model and inputs: small pseudo-random values in every parameter.
+  for (const LayerPlan &lp : m.layers) {
+    for (const ConvSpec &c : lp.convs) {
+      HIP_TRY(launch_fill_pattern(m.bf16, pk + c.pk_w, (int64_t)c.cout * c.Kp, 0x1234u + (uint32_t)c.pk_w,
+                                  1.0f / std::sqrt((float)c.K), s));
+      HIP_TRY(launch_fill_pattern(false, pk + c.pk_b, c.cout, 0x77u + (uint32_t)c.pk_b, 0.05f, s));
+    }
+    for (const Extra &e : lp.extras)
+      HIP_TRY(launch_fill_pattern(false, pk + e.pk, e.n, 0x99u + (uint32_t)e.pk, 0.05f, s));
+  }
+  HIP_TRY(launch_fill_pattern(m.bf16, img, (int64_t)batch * m.input.elems(), 0xabcdu, 1.0f, s));
+
+  constexpr int kWarm = 5, kRuns = 20;
+  std::vector<hipEvent_t> ev;
+  std::vector<std::vector<float>> t(n, std::vector<float>());
+  std::vector<float> acc(n);
+  const int nchunks = (batch + chunk - 1) / chunk;
+  const int per_pass = 2 * n * nchunks;
+  ev.resize(per_pass);
+  for (auto &e : ev) HIP_TRY(hipEventCreate(&e));
+  int rc = HAPI_OK;
+  for (int it = 0; it < kWarm + kRuns && rc == HAPI_OK; ++it) {
+    int idx = 0;
+    auto cb = [&](int layer, bool begin) {
+      (void)layer;
+      (void)begin;
+      (void)hipEventRecord(ev[idx++], s);
+    };
+    rc = run_batch(desc, m, pk, img, batch, n, nullptr, ws, chunk, cb);
+    if (rc != HAPI_OK) break;
+    if (hipEventSynchronize(ev[idx - 1]) != hipSuccess) {
+      rc = fail(HAPI_E_DEVICE, "hipEventSynchronize failed");
+      break;
+    }
+    if (it < kWarm) continue;
+    std::fill(acc.begin(), acc.end(), 0.0f);
+    for (int ci = 0; ci < nchunks; ++ci)
+      for (int k = 0; k < n; ++k) {
+        float ms = 0.0f;
+        (void)hipEventElapsedTime(&ms, ev[ci * 2 * n + 2 * k], ev[ci * 2 * n + 2 * k + 1]);
+        acc[k] += ms;
+      }
+    for (int k = 0; k < n; ++k) t[k].push_back(acc[k]);
+  }
+  for (auto &e : ev) (void)hipEventDestroy(e);
+  if (rc != HAPI_OK) return rc;
+  out_us[0] = 0.0f;
+  for (int k = 0; k < n; ++k) {
+    std::vector<float> v = t[k];
+    std::nth_element(v.begin(), v.begin() + v.size() / 2, v.end());
+    out_us[k + 1] = v[v.size() / 2] * 1000.0f;
+  }
+  return HAPI_OK;
+}
+
+int hapi_stats_enable(int32_t enable) {
+  std::lock_guard<std::mutex> g(g_stats_mu);
+  for (StatRec &r : g_recs) {
+    g_pool.push_back(r.a);
+    g_pool.push_back(r.b);
+  }
+  g_recs.clear();
+  g_stats_on = enable != 0;
+  return HAPI_OK;
+}
+
+int hapi_stats_collect(hapi_kernel_stat *out, int32_t max_entries) {
+  std::lock_guard<std::mutex> g(g_stats_mu);
+  if (!out || max_entries < 0) return fail(HAPI_E_INVAL, "out is NULL");
+  hapi_kernel_stat acc[F_COUNT];
+  std::memset(acc, 0, sizeof acc);
+  for (int f = 0; f < F_COUNT; ++f) std::snprintf(acc[f].name, sizeof acc[f].name, "%s", kFamily[f]);
+  for (StatRec &r : g_recs) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return fail(HAPI_E_DEVICE, "hipEventSynchronize failed");
+    float ms = 0.0f;
+    (void)hipEventElapsedTime(&ms, r.a, r.b);
+    acc[r.fam].launches += 1;
+    acc[r.fam].total_ms += ms;
+    acc[r.fam].flops += r.flops;
+    acc[r.fam].bytes += r.bytes;
+  }
+  int nout = 0;
+  for (int f = 0; f < F_COUNT; ++f) {
+    if (acc[f].launches == 0) continue;
+    if (nout < max_entries) out[nout] = acc[f];
+    ++nout;
+  }
+  return nout;
+}
+
+const char *hapi_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

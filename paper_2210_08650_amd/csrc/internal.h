@@ -1,0 +1,72 @@
+// Internal declarations shared by the host runtime and the HIP kernels of libhapi.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "hapi.h"
+
+namespace hapi {
+
+// ---------------------------------------------------------------- kernels
+
+// Where a convolution reads its input from.
+enum Loader : int {
+  LD_NHWC = 0,       // NHWC activation, cin % 64 == 0 (bf16) / cin % 16 == 0 (f32)
+  LD_GEMM = 1,       // row-major [M, K] matrix: a 1x1 / stride 1 / pad 0 convolution
+  LD_NCHW = 2,       // NCHW images, any geometry, element gather (first layer)
+  LD_NCHW_PATCH = 3  // NCHW images, non-overlapping patches with k % 8 == 0 (bf16)
+};
+
+// One convolution / linear layer as an implicit GEMM:
+//   y[m, n] = act( sum_k A[m, k] * Wp[n, k] + bias[n] (+ res[m, n]) )
+// m = (image, ho, wo) in NHWC order, n = output channel,
+// k = (kh, kw, c) for NHWC inputs and (c, kh, kw) for NCHW inputs.
+struct ConvArgs {
+  const void *x;       // input activation
+  const void *w;       // packed weights [N][Kp], zero padded beyond K
+  const float *bias;   // [N] float32, may be null
+  const void *res;     // residual [M][ldr] in the activation type, may be null
+  void *y;             // output [M][ldc]
+  int n_img, H, W, C;  // input geometry
+  int Ho, Wo;
+  int kh, kw, stride, pad;
+  int M, N, K, Kp;
+  int ldc, ldr;
+  int relu, gelu;
+};
+
+hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s);
+hipError_t launch_conv_f32(const ConvArgs &a, Loader ld, hipStream_t s);
+
+// Elementwise / memory-bound kernels; `bf16` selects the activation type.
+hipError_t launch_maxpool(bool bf16, const void *x, void *y, int n, int H, int W, int C, int k,
+                          int stride, int pad, int Ho, int Wo, hipStream_t s);
+hipError_t launch_avgpool(bool bf16, const void *x, void *y, int n, int H, int W, int C, int k,
+                          int stride, int Ho, int Wo, hipStream_t s);
+// [n, HW, C] <-> [n, C, HW]
+hipError_t launch_nhwc_to_nchw(bool bf16, const void *x, void *y, int n, int HW, int C,
+                               hipStream_t s);
+hipError_t launch_nchw_to_nhwc(bool bf16, const void *x, void *y, int n, int HW, int C,
+                               hipStream_t s);
+hipError_t launch_copy(const void *x, void *y, size_t bytes, hipStream_t s);
+hipError_t launch_fill_pattern(bool bf16, void *y, int64_t n, uint32_t seed, float scale,
+                               hipStream_t s);
+hipError_t launch_tokens(const void *patch, const float *cls, const float *pos, void *y, int n,
+                         int T, int D, hipStream_t s);
+hipError_t launch_layernorm(const void *x, const float *gamma, const float *beta, void *y,
+                            int64_t rows, int D, float eps, hipStream_t s);
+hipError_t launch_attention(const void *qkv, void *out, int n, int T, int D, int heads,
+                            hipStream_t s);
+// Weight packing.  nchw_order: k = (c, kh, kw), else k = (kh, kw, c).
+hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, const float *gamma,
+                            const float *beta, const float *mean, const float *var, int N, int C,
+                            int kh, int kw, int Kp, bool nchw_order, void *wp, float *bias_out,
+                            hipStream_t s);
+hipError_t launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s);
+
+constexpr int kAttnMaxTokens = 256;
+constexpr int kHeadDim = 64;
+
+}  // namespace hapi

@@ -1,0 +1,114 @@
+"""Bit-exact checks of every convolution loader and tile shape on the GPU.
+
+With small-integer images, weights and biases every partial sum is an integer
+far below 2^24, so the kernels' fp32 accumulation is exact in any order and the
+only rounding is the single round-to-nearest-even of the output to the model
+dtype.  The GPU output must therefore equal the oracle's exact result rounded
+once, bit for bit.  Max pooling is exact for any values.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2210_08650_amd as H
+from paper_2210_08650_amd import models as PM
+import synth
+from oracle import layers as L
+from tests.hip_harness import Runner, bf16_round, images_for
+
+pytestmark = pytest.mark.gpu
+
+
+def _int_conv_case(seed, dtype, pre_pool, C, N, k, s, p, HW, batch, relu=True, lo=-1, hi=1):
+    layers = ([PM.maxpool(1, 1)] if pre_pool else []) + [PM.conv(C, N, k, s, p, bias=True, relu=relu)]
+    w = synth.small_ints(seed, (N, C, k, k), lo, hi)
+    b = synth.small_ints(seed + 1, (N,), -3, 3)
+    x = synth.small_ints(seed + 2, (batch, C, HW, HW), -2, 2)
+    r = Runner(layers, dtype, [w, b], (C, HW, HW))
+    xd, xv = images_for(dtype, x)
+    got = r.extract_np(xd, len(layers))
+    ref = L.conv2d(xv, w, b, s, p)
+    if relu:
+        ref = np.maximum(ref, 0)
+    ref = ref.astype(np.float32)
+    if dtype == H.HAPI_BF16:
+        ref = bf16_round(ref)
+    print(f"case seed={seed} C={C} N={N} k={k} s={s} p={p} HW={HW} B={batch}", flush=True)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref), np.abs(got - ref).max()
+
+
+# (pre_pool, C, N, k, s, p, HW, batch): pre_pool routes the conv through the
+# NHWC loaders (a 1x1 identity pool first); otherwise it reads NCHW images.
+BF16_CASES = [
+    (False, 3, 64, 3, 1, 1, 23, 3),      # NCHW gather, K = 27 padded to 64, ragged M
+    (False, 3, 64, 7, 2, 3, 37, 2),      # stem geometry, K = 147
+    (False, 3, 96, 11, 4, 2, 63, 2),     # 11x11 / 4, K = 363, ragged N tile
+    (False, 3, 128, 16, 16, 0, 64, 3),   # patch loader (16-byte NCHW rows)
+    (True, 64, 128, 3, 1, 1, 15, 3),     # NHWC 3x3
+    (True, 128, 192, 3, 2, 1, 17, 2),    # NHWC 3x3 / 2, N = 192
+    (True, 64, 256, 1, 2, 0, 14, 3),     # 1x1 / 2 shortcut geometry
+    (True, 128, 64, 1, 1, 0, 21, 2),     # GEMM loader, N = 64 tile
+    (True, 64, 256, 1, 1, 0, 128, 4),    # M = 65536: 256 x 128 tiles
+]
+
+
+@pytest.mark.parametrize("case", BF16_CASES)
+def test_conv_bf16_integer_exact(case):
+    _int_conv_case(100 + BF16_CASES.index(case) * 10, H.HAPI_BF16, *case)
+
+
+F32_CASES = [
+    (False, 3, 64, 11, 4, 2, 47, 2),     # AlexNet conv1 geometry
+    (False, 3, 32, 3, 1, 1, 19, 3),
+    (True, 64, 192, 5, 1, 2, 13, 2),     # AlexNet conv2 geometry
+    (True, 192, 96, 3, 1, 1, 13, 2),
+    (True, 32, 48, 1, 1, 0, 9, 3),       # GEMM loader
+]
+
+
+@pytest.mark.parametrize("case", F32_CASES)
+def test_conv_f32_integer_exact(case):
+    _int_conv_case(300 + F32_CASES.index(case) * 10, H.HAPI_F32, *case, lo=-3, hi=3)
+
+
+@pytest.mark.parametrize("dtype", [H.HAPI_BF16, H.HAPI_F32])
+@pytest.mark.parametrize("k,s,p", [(3, 2, 0), (3, 2, 1), (2, 2, 0)])
+def test_maxpool_exact(dtype, k, s, p):
+    x = synth.images(7, 3, 64, 29, 29)
+    xd, xv = images_for(dtype, x)
+    r = Runner([PM.maxpool(k, s, p)], dtype, [], (64, 29, 29))
+    got = r.extract_np(xd, 1)
+    ref = L.maxpool2d(xv, k, s, p).astype(np.float32)
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("dtype", [H.HAPI_BF16, H.HAPI_F32])
+def test_global_avgpool(dtype):
+    x = synth.images(8, 3, 256, 7, 7)
+    xd, xv = images_for(dtype, x)
+    r = Runner([PM.avgpool()], dtype, [], (256, 7, 7))
+    got = r.extract_np(xd, 1)
+    ref = L.avgpool_global(xv)
+    # fp32 summation of 49 terms: |error| <= 49 * 2^-24 * mean|x|; bf16 adds
+    # one output rounding of at most 2^-9 relative.
+    scale = np.abs(xv).mean(axis=(2, 3), keepdims=True)
+    tol = 49 * 2.0 ** -24 * scale + (2.0 ** -9 * np.abs(ref) if dtype == H.HAPI_BF16 else 0)
+    assert np.all(np.abs(got - ref) <= tol), np.abs(got - ref).max()
+
+
+def test_identity_kernel_conv_is_exact_on_random_values():
+    # W = delta(o, c) at the kernel centre: y = x exactly, in bf16 and fp32.
+    for dtype in (H.HAPI_BF16, H.HAPI_F32):
+        C = 64
+        w = np.zeros((C, C, 3, 3), np.float32)
+        for c in range(C):
+            w[c, c, 1, 1] = 1.0
+        x = synth.images(9, 2, C, 11, 11)
+        xd, xv = images_for(dtype, x)
+        r = Runner([PM.maxpool(1, 1), PM.conv(C, C, 3, 1, 1, bias=True, relu=False)], dtype,
+                   [w, np.zeros(C, np.float32)], (C, 11, 11))
+        assert np.array_equal(r.extract_np(xd, 2), xv)
+        r2 = Runner([PM.maxpool(1, 1), PM.conv(C, C, 3, 2, 1, bias=True, relu=False)], dtype,
+                    [w, np.zeros(C, np.float32)], (C, 11, 11))
+        assert np.array_equal(r2.extract_np(xd, 2), xv[:, :, ::2, ::2])

@@ -1,0 +1,147 @@
+"""Parity of the HIP feature-extraction path with the CPU oracle, per model.
+
+Every split boundary of each evaluated model is compared with the oracle on
+the same synthetic images and weights, at relative L2 <= 1e-4 for the fp32
+path and <= 2e-2 for the bf16 paths (bf16 weights and activations, fp32
+accumulation, one rounding per materialised tensor).  Batch partitioning
+(storage-side batch adaptation) must not change a single bit.
+"""
+import numpy as np
+import pytest
+
+import paper_2210_08650_amd as H
+from paper_2210_08650_amd import models as PM
+import synth
+from oracle import models as OM
+from tests.hip_harness import Runner, images_for, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+TOL = {H.HAPI_F32: 1e-4, H.HAPI_BF16: 2e-2}
+
+
+def _setup(name, seed, batch, layers=None, omodel=None, in_shape=(3, 224, 224), params=None):
+    layers = layers or PM.FACTORIES[name]()
+    om = omodel or OM.build(name)
+    dtype = H.HAPI_F32 if name == "alexnet" else H.HAPI_BF16
+    ps = params if params is not None else synth.params(seed, om.manifest())
+    imgs = synth.images(seed, batch, *in_shape)
+    xd, xv = images_for(dtype, imgs)
+    return Runner(layers, dtype, ps, in_shape), om, ps, xd, xv, dtype
+
+
+@pytest.mark.parametrize("name,batch", [("alexnet", 4), ("resnet18", 3), ("resnet50", 2),
+                                        ("vgg16", 2), ("vit_b16", 2)])
+def test_every_split_matches_oracle(name, batch):
+    r, om, ps, xd, xv, dtype = _setup(name, 10 + len(name), batch)
+    outs = om.forward(ps, xv, om.n_layers, collect=True)
+    for split in range(0, om.n_layers + 1):
+        got = r.extract_np(xd, split)
+        err = rel_l2(got, outs[split])
+        print(f"{name} split {split}: rel_l2 {err:.3e}", flush=True)
+        assert got.shape == outs[split].shape
+        if split == 0:
+            assert np.array_equal(got, xv)
+        assert err <= TOL[dtype], (split, err)
+
+
+@pytest.mark.parametrize("name,split,chunks", [("resnet18", 8, (1, 2, 5)),
+                                                ("alexnet", 8, (1, 3)),
+                                                ("vit_b16", 4, (1, 3))])
+def test_chunking_is_bit_exact(name, split, chunks):
+    r, _, _, xd, _, _ = _setup(name, 40, 5)
+    whole = r.extract_np(xd, split, chunk=0)
+    for c in chunks:
+        assert H.hapi_chunk_count(r.desc.set(chunk=c), 5) == -(-5 // c)
+        assert np.array_equal(r.extract_np(xd, split, chunk=c), whole), c
+    # row i depends on image i only
+    single = r.extract_np(xd[3:4].contiguous(), split)
+    assert np.array_equal(single[0], whole[3])
+
+
+def _vit_small(depth=2):
+    return (PM.vit(image=64, patch=16, dim=128, heads=2, mlp=256, depth=depth),
+            OM.vit(image=64, patch=16, dim=128, heads=2, mlp=256, depth=depth, name="vit_small"))
+
+
+@pytest.mark.parametrize("branch", ["attention", "mlp"])
+def test_vit_sub_layer_branches(branch):
+    # Isolate one branch: zero the other branch's output projection and scale
+    # this branch's output projection up, so that the block's change of the
+    # residual stream is this branch alone and dominates the stream (the delta
+    # of two bf16-rounded streams is otherwise floored by their rounding).
+    # The scaled branch still carries the attention pattern, so a wrong score
+    # scale or a mixed-up head moves it far beyond the tolerance.
+    for layers, om, shape in (_vit_small() + ((3, 64, 64),),
+                              (PM.vit(depth=8), OM.vit(depth=8), (3, 224, 224))):
+        ps = synth.params(60, om.manifest())
+        per_block, start = 12, 4  # after patch weight, bias, class token, position embedding
+        nblk = sum(1 for L in layers if L["kind"] == H.HAPI_VIT_BLOCK)
+        for b in range(nblk):
+            base = start + b * per_block
+            zero, scale = ((base + 10, base + 11), (base + 4, base + 5)) if branch == "attention" \
+                else ((base + 4, base + 5), (base + 10, base + 11))
+            for i in zero:
+                ps[i] = np.zeros_like(ps[i])
+            for i in scale:
+                ps[i] = (ps[i] * 16.0).astype(np.float32)
+        r = Runner(layers, H.HAPI_BF16, ps, shape)
+        imgs = synth.images(61, 1, *shape)
+        xd, xv = images_for(H.HAPI_BF16, imgs)
+        outs = om.forward(ps, xv, om.n_layers - 1, collect=True)
+        for blk in sorted({1, nblk}):
+            k = 2 + blk
+            d_ref = outs[k] - outs[k - 1]
+            d_got = r.extract_np(xd, k) - r.extract_np(xd, k - 1)
+            ratio = np.linalg.norm(d_ref) / np.linalg.norm(outs[k - 1])
+            err = rel_l2(d_got, d_ref)
+            print(f"{branch} branch, block {blk}, tokens {outs[k].shape[1]}: |delta|/|x| "
+                  f"{ratio:.2f}, rel_l2 {err:.3e}", flush=True)
+            assert err <= 2e-2
+
+
+def test_batch_of_one_and_ragged_tail():
+    r, om, ps, xd, xv, _ = _setup("resnet50", 70, 3)
+    ref = om.forward(ps, xv[:1], 18)
+    assert rel_l2(r.extract_np(xd[:1].contiguous(), 18), ref) <= 2e-2
+    a = r.extract_np(xd, 18, chunk=2)       # partitions of 2 + 1
+    b = r.extract_np(xd, 18, chunk=0)
+    assert np.array_equal(a, b)
+
+
+def test_exact_workspace_and_nomem_leaves_output_untouched():
+    import torch
+    r, _, _, xd, _, _ = _setup("resnet18", 71, 2)
+    r.extract(xd, 8)  # exact-size workspace succeeds
+    out = torch.full((2,) + r.out_shape(8), 7.0, dtype=r.tdtype, device="cuda")
+    need = H.hapi_workspace_bytes(r.desc.set(chunk=0), 2, 8)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    r.desc.set(workspace=ws, workspace_bytes=need - 1)
+    with pytest.raises(H.HapiError) as e:
+        H.hapi_extract(r.desc, r.packed, xd, 2, 8, out)
+    assert e.value.code == H.HAPI_E_NOMEM
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())
+
+
+def test_profile_layers_times_every_layer():
+    import torch
+    d = H.Desc(PM.resnet18(), H.HAPI_BF16, stream=torch.cuda.current_stream(), chunk=16)
+    need = H.hapi_workspace_bytes(d, 32, d.n_layers, True)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    d.set(workspace=ws, workspace_bytes=need)
+    b, us = H.hapi_profile_layers(d, 32, True)
+    assert us[0] == 0.0 and all(t > 0 for t in us[1:]), us
+    assert b == H.hapi_profile_layers(d, 32)[0]
+
+
+def test_kernel_stats_count_launches():
+    r, _, _, xd, _, _ = _setup("resnet50", 72, 2)
+    H.hapi_stats_enable(True)
+    r.extract(xd, 18)
+    st = {s["name"]: s for s in H.hapi_stats_collect()}
+    H.hapi_stats_enable(False)
+    # stem + 16 blocks x 3 convs + 4 shortcut convs
+    assert st["conv_bf16"]["launches"] == 1 + 48 + 4
+    assert st["conv_bf16"]["total_ms"] > 0 and st["conv_bf16"]["flops"] > 0
+    assert st["maxpool"]["launches"] == 1
