@@ -54,6 +54,7 @@ struct Act {  // per-image activation, stored NHWC (tokens: h = T, w = 1, c = D)
 struct ConvSpec {
   int cin, cout, k, stride, pad;
   bool bias, bn;
+  bool s2d;  // stride-2 stem on 2x2 space-to-depth cells (first layer, few channels)
   int K, Kp;
   int64_t raw_w, raw_b, raw_bn;  // float offsets into the raw buffer (-1: absent)
   int64_t pk_w, pk_b;            // byte offsets into the packed buffer
@@ -99,12 +100,14 @@ int analyze(const hapi_model_desc *d, Model &m) {
   Act cur = m.input;
   int64_t raw = 0, pk = 0;
 
-  auto add_conv = [&](LayerPlan &lp, int cin, int cout, int k, int s, int p, bool bias, bool bn) {
+  auto add_conv = [&](LayerPlan &lp, int cin, int cout, int k, int s, int p, bool bias, bool bn,
+                      bool s2d = false) {
     ConvSpec c{};
     c.cin = cin; c.cout = cout; c.k = k; c.stride = s; c.pad = p; c.bias = bias; c.bn = bn;
-    c.K = cin * k * k;
+    c.s2d = s2d;
+    c.K = s2d ? ((k + 1) / 2) * ((k + 1) / 2) * kS2DChannels : cin * k * k;
     c.Kp = (c.K + kq - 1) / kq * kq;
-    c.raw_w = raw; raw += (int64_t)cout * c.K;
+    c.raw_w = raw; raw += (int64_t)cout * cin * k * k;
     c.raw_b = -1; c.raw_bn = -1;
     if (bias) { c.raw_b = raw; raw += cout; }
     if (bn) { c.raw_bn = raw; raw += 4 * (int64_t)cout; }
@@ -138,8 +141,13 @@ int analyze(const hapi_model_desc *d, Model &m) {
         if (ho < 1 || wo < 1) return fail(HAPI_E_INVAL, "layer %d: empty conv output", li + 1);
         if (!first && !nhwc_ok(L.cin))
           return fail(HAPI_E_UNSUPPORTED, "layer %d: conv with cin %% %d != 0 after the first layer", li + 1, kq);
-        add_conv(lp, L.cin, L.cout, L.k, L.stride, L.pad, L.has_bias != 0, L.has_bn != 0);
+        // A stride-2 first layer over <= 4 channels whose receptive field spans
+        // 4 x 4 cells of 2 x 2 pixels runs on the space-to-depth layout.
+        const bool s2d = first && m.bf16 && L.stride == 2 && L.cin <= 4 && (L.k + 1) / 2 == 4 &&
+                         L.cout % 8 == 0;
+        add_conv(lp, L.cin, L.cout, L.k, L.stride, L.pad, L.has_bias != 0, L.has_bn != 0, s2d);
         lp.out = Act{L.cout, ho, wo, false};
+        if (s2d) lp.tmp_elems = (int64_t)(ho + 3) * (wo + 3) * kS2DChannels;
         if (first) m.first_reads_nchw = true;
         break;
       }
@@ -366,7 +374,17 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
   a.relu = relu;
   a.gelu = gelu;
   Loader ld;
-  if (nchw_input) {
+  if (cs.s2d) {
+    // x is the space-to-depth buffer: a stride-1 4 x 4 convolution over cells.
+    const int k2 = (cs.k + 1) / 2;
+    a.H = a.Ho + k2 - 1;
+    a.W = a.Wo + k2 - 1;
+    a.C = kS2DChannels;
+    a.kh = a.kw = k2;
+    a.stride = 1;
+    a.pad = 0;
+    ld = LD_S2D;
+  } else if (nchw_input) {
     const bool vec_ok = c.m.bf16 && cs.k % 8 == 0 && cs.stride % 8 == 0 && cs.pad == 0 &&
                         in.w % 8 == 0 && ((uintptr_t)x % 16) == 0;
     ld = vec_ok ? LD_NCHW_PATCH : LD_NCHW;
@@ -408,8 +426,21 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
     switch (L.kind) {
       case HAPI_CONV:
       case HAPI_PATCH_EMBED: {
-        const int o = free_slot();
-        HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[o], nullptr,
+        const ConvSpec &cs = lp.convs[0];
+        const void *src = cur;
+        int o = free_slot();
+        if (cs.s2d) {
+          const int ho = lp.out.h, wo = lp.out.w;
+          HIP_TRY(timed(c.s, F_LAYOUT, 0.0,
+                        (double)nb * (lp.in.elems() + (int64_t)(ho + 3) * (wo + 3) * kS2DChannels) * m.esz,
+                        [&] {
+                          return launch_space_to_depth(cur, c.slot[o], nb, lp.in.c, lp.in.h, lp.in.w,
+                                                       cs.pad, ho + 3, wo + 3, c.s);
+                        }));
+          src = c.slot[o];
+          o = free_slot(o);
+        }
+        HIP_TRY(run_conv(c, cs, src, lp.in, nb, c.slot[o], nullptr,
                          L.kind == HAPI_CONV && L.relu, false, nchw_in));
         cur = c.slot[o];
         cur_slot = o;
@@ -628,9 +659,10 @@ int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void
     const bool nchw = li == 0 && m.first_reads_nchw;
     for (const ConvSpec &c : lp.convs) {
       const float *bn = c.raw_bn >= 0 ? raw + c.raw_bn : nullptr;
+      const PackOrder order = c.s2d ? PACK_S2D : nchw ? PACK_CKHKW : PACK_KHKWC;
       HIP_TRY(launch_pack_conv(m.bf16, raw + c.raw_w, c.raw_b >= 0 ? raw + c.raw_b : nullptr,
                                bn, bn ? bn + c.cout : nullptr, bn ? bn + 2 * c.cout : nullptr,
-                               bn ? bn + 3 * c.cout : nullptr, c.cout, c.cin, c.k, c.k, c.Kp, nchw,
+                               bn ? bn + 3 * c.cout : nullptr, c.cout, c.cin, c.k, c.k, c.Kp, order,
                                pk + c.pk_w, reinterpret_cast<float *>(pk + c.pk_b), s));
     }
     for (const Extra &e : lp.extras)

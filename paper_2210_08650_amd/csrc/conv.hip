@@ -14,6 +14,8 @@
 // Every output element's reduction visits the k-tiles in order and, inside a
 // tile, the MFMA k-steps in order, independent of the tile shape (BM, BN) and
 // of M.  Results are therefore bit-identical for any batch split.
+#include <cstdlib>
+
 #include "internal.h"
 
 namespace hapi {
@@ -271,12 +273,14 @@ struct PipeSmem {
       (STAGES * kStage * 2 > BM * kCPitch * 4) ? STAGES * kStage * 2 : BM * kCPitch * 4;
 };
 
-template <int BM, int BN, int STAGES, int LD>
-__global__ __launch_bounds__(kThreads) void conv_bf16_pipe_kernel(ConvArgs a) {
-  constexpr int WN = 2;
-  constexpr int TM = BM / 64, TN = BN / 64;
-  constexpr int NA = BM / 32, NB = BN / 32;  // DMA instructions per thread per stage
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED>
+__global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a) {
+  constexpr int NT = WM * WN * 64;                    // threads: WM x WN waves
+  constexpr int TM = BM / (WM * 32), TN = BN / (WN * 32);
+  constexpr int NA = BM * 8 / NT, NB = BN * 8 / NT;   // DMA instructions per thread per stage
+  constexpr int KS = BK / 16;                         // MFMA k-steps per k-tile
   using SM = PipeSmem<BM, BN, STAGES>;
+  static_assert(TM >= 1 && TN >= 1 && NA >= 1 && NB >= 1, "tile");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
   static_assert((STAGES - 2) * (NA + NB) < 64, "vmcnt range");
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[SM::kBytes];
@@ -287,62 +291,88 @@ __global__ __launch_bounds__(kThreads) void conv_bf16_pipe_kernel(ConvArgs a) {
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int kc = (lane & 7) ^ (lane >> 3);  // logical chunk this lane moves (see swizzle)
+  const int kc8 = ((lane & 7) ^ (lane >> 3)) * 8;  // first k of the chunk this lane moves
   const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero_chunk);
   const uint16_t *x = static_cast<const uint16_t *>(a.x);
   const uint16_t *wp = static_cast<const uint16_t *>(a.w);
 
-  RowState rs[NA];
+  // Per-row gather state, computed once: element offset of the row's first
+  // tap (may point into padding), and the tap origin for bounds checks.
+  int roff[NA], rhi[NA], rwi[NA];
 #pragma unroll
-  for (int i = 0; i < NA; ++i) rs[i] = make_row<LD>(a, m0 + (wave * NA + i) * 8 + (lane >> 3));
-  const uint16_t *bptr[NB];
+  for (int i = 0; i < NA; ++i) {
+    const RowState r = make_row<LD>(a, m0 + (wave * NA + i) * 8 + (lane >> 3));
+    rhi[i] = r.hi0;
+    rwi[i] = r.wi0;
+    if (LD == LD_NHWC || LD == LD_S2D) roff[i] = r.base + (r.hi0 * a.W + r.wi0) * a.C + kc8;
+    else if (LD == LD_GEMM) roff[i] = r.base + kc8;
+    else roff[i] = r.base;
+  }
+  int boffs[NB];
+  bool bok[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int n = n0 + (wave * NB + j) * 8 + (lane >> 3);
-    bptr[j] = n < a.N ? wp + (size_t)n * a.Kp + kc * 8 : nullptr;
+    bok[j] = n < a.N;
+    boffs[j] = (bok[j] ? n : 0) * a.Kp + kc8;
   }
+  const int nk = a.Kp / BK;
 
+  // Moves k-tile kt (< nk) into stage st.  Only per-lane conditions select
+  // the zero chunk, so the address arithmetic stays branch-free.
   auto issue = [&](int kt, int st) {
     uint16_t *As = smem + st * SM::kStage;
     uint16_t *Bs = As + BM * BK;
     const int kbase = kt * BK;
-    int kh_ = 0, kw_ = 0, c0 = 0;
+    int kh_ = 0, kw_ = 0, tapoff = 0;
     if (LD == LD_NHWC) {
       const int tap = kbase / a.C;
-      c0 = kbase - tap * a.C + kc * 8;
       kh_ = tap / a.kw;
       kw_ = tap - kh_ * a.kw;
+      tapoff = (kh_ * a.W + kw_) * a.C + (kbase - tap * a.C);
     }
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
-      const uint16_t *src = zero;
-      const RowState &r = rs[i];
+      bool ok;
+      int off;
       if (LD == LD_GEMM) {
-        if (r.hi0 >= 0) src = x + r.base + kbase + kc * 8;
+        ok = rhi[i] >= 0;
+        off = roff[i] + kbase;
       } else if (LD == LD_NHWC) {
-        const int hi = r.hi0 + kh_, wi = r.wi0 + kw_;
-        if ((unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W)
-          src = x + r.base + (hi * a.W + wi) * a.C + c0;
-      } else {  // LD_NCHW_PATCH
-        const int k0 = kbase + kc * 8;
-        if (r.hi0 > -(1 << 27) && k0 < a.K) {
-          const int khw = a.kh * a.kw;
-          const int c = k0 / khw, rem = k0 - c * khw;
-          const int u = rem / a.kw, vv = rem - u * a.kw;
-          src = x + r.base + (c * a.H + r.hi0 + u) * a.W + r.wi0 + vv;
-        }
+        ok = (unsigned)(rhi[i] + kh_) < (unsigned)a.H && (unsigned)(rwi[i] + kw_) < (unsigned)a.W;
+        off = roff[i] + tapoff;
+      } else if (LD == LD_S2D) {
+        // k-tile kt is the contiguous run of cell row du = kt (kw x 16 = 64 elements)
+        ok = rhi[i] >= 0;
+        off = roff[i] + kt * a.W * a.C;
+      } else {  // LD_NCHW_PATCH: k = (c, u, v), 8 | kw
+        const int k0 = kbase + kc8;
+        const int khw = a.kh * a.kw;
+        const int c = k0 / khw, rem = k0 - c * khw;
+        const int u = rem / a.kw, vv = rem - u * a.kw;
+        ok = rhi[i] > -(1 << 27) && k0 < a.K;
+        off = roff[i] + (c * a.H + rhi[i] + u) * a.W + rwi[i] + vv;
       }
+      const uint16_t *src = ok ? x + off : zero;
       __builtin_amdgcn_global_load_lds(src, LDS_PTR(As + (wave * NA + i) * 512), 16, 0, 0);
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      const uint16_t *src = bptr[j] ? bptr[j] + kbase : zero;
+      const uint16_t *src = bok[j] ? wp + boffs[j] + kbase : zero;
       __builtin_amdgcn_global_load_lds(src, LDS_PTR(Bs + (wave * NB + j) * 512), 16, 0, 0);
     }
   };
 
   const int wm = wave / WN, wn = wave % WN;
   const int lrow = lane & 31, lh = lane >> 5;
+  // Fragment offsets inside a stage; k-step ks reads logical chunk 2 ks + lh,
+  // stored at physical chunk (2 ks + lh) ^ (row & 7), and row & 7 == lrow & 7.
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) aoff[i] = (wm * TM * 32 + i * 32 + lrow) * BK;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) boff[j] = BM * BK + (wn * TN * 32 + j * 32 + lrow) * BK;
+  const int sw = lrow & 7;
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -352,43 +382,74 @@ __global__ __launch_bounds__(kThreads) void conv_bf16_pipe_kernel(ConvArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = a.Kp / BK;
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s, s);
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < nk) issue(st, st);
 
-  for (int kt = 0; kt < nk; ++kt) {
-    // Tiles issued after kt that may stay in flight: min(STAGES - 2, nk - 1 - kt).
-    const int ahead = nk - 1 - kt;
-    if (STAGES >= 4 && ahead >= 2) wait_vmcnt<(STAGES >= 4 ? 2 : 0) * (NA + NB)>();
-    else if (STAGES >= 3 && ahead >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * (NA + NB)>();
-    else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-
-    const uint16_t *As = smem + (kt % STAGES) * SM::kStage;
-    const uint16_t *Bs = As + BM * BK;
+  bf16x8_t af[2][TM], bfr[2][TN];
+  // One k-tile from LDS stage S: 4 MFMA k-steps, the next step's fragments
+  // read while the current step's MFMAs run.  `pre` issues the DMA of a later
+  // k-tile after the first fragments are read.
+  auto run_tile = [&](const uint16_t *S, auto &&pre) {
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8_t af[TM], bfr[TN];
+    for (int i = 0; i < TM; ++i)
+      af[0][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ((lh ^ sw) * 8));
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * TM * 32 + i * 32 + lrow;
-        af[i] = *reinterpret_cast<const bf16x8_t *>(As + r * BK + (((2 * ks + lh) ^ (r & 7)) * 8));
-      }
+    for (int j = 0; j < TN; ++j)
+      bfr[0][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ((lh ^ sw) * 8));
+    pre();
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * TN * 32 + j * 32 + lrow;
-        bfr[j] = *reinterpret_cast<const bf16x8_t *>(Bs + r * BK + (((2 * ks + lh) ^ (r & 7)) * 8));
+    for (int ks = 0; ks < KS; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < KS) {
+        const int ch = ((2 * (ks + 1) + lh) ^ sw) * 8;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[cur ^ 1][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfr[cur ^ 1][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  int kt = 0;
+  // Steady state: STAGES - 2 younger tiles in flight at the wait, and the
+  // tile STAGES - 1 ahead is issued every iteration.
+  for (; kt + STAGES - 1 < nk; ++kt) {
+    wait_vmcnt<(STAGES - 2) * (NA + NB)>();
+    __builtin_amdgcn_s_barrier();
+    run_tile(smem + (kt % STAGES) * SM::kStage,
+             [&] { issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES); });
+    if (SCHED) {
+      // Spread the next k-steps' LDS reads and the DMA issue (address
+      // arithmetic + global_load_lds) between the MFMAs of this k-tile.
+      constexpr int NMF = KS * TM * TN;
+      constexpr int NRD = (KS - 1) * (TM + TN);
+      constexpr int NDMA = NA + NB;
+#pragma unroll
+      for (int q = 0; q < NMF; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
+        if (q < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // DS read
+        if (q < NDMA) {
+          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);               // VALU
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);               // VMEM (DMA)
+        }
+      }
     }
   }
-
+  // Drain: no more tiles to issue.
+  for (; kt < nk; ++kt) {
+    if (STAGES >= 3 && nk - 1 - kt >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * (NA + NB)>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    run_tile(smem + (kt % STAGES) * SM::kStage, [] {});
+  }
   // Epilogue: stage the fp32 tile in LDS, then each thread finishes 8
   // consecutive output channels of a row and stores them as one 16-byte write.
   __syncthreads();
@@ -405,7 +466,7 @@ __global__ __launch_bounds__(kThreads) void conv_bf16_pipe_kernel(ConvArgs a) {
       }
   __syncthreads();
   constexpr int CPR = BN / 8;             // 8-column chunks per row
-  constexpr int RPP = kThreads / CPR;     // rows per pass
+  constexpr int RPP = NT / CPR;           // rows per pass
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
   if (n >= a.N) return;
@@ -448,24 +509,44 @@ hipError_t launch_bf16_cfg(const ConvArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int STAGES, int LD>
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED = 0>
 hipError_t launch_pipe_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((conv_bf16_pipe_kernel<BM, BN, STAGES, LD>), dim3(tiles), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED>), dim3(tiles),
+                     dim3(WM * WN * 64), 0, s, a);
   return hipGetLastError();
+}
+
+// Tuning override: HAPI_CONV_CFG=<index> forces one tile configuration.
+int forced_cfg() {
+  static const int v = [] {
+    const char *e = getenv("HAPI_CONV_CFG");
+    return e ? atoi(e) : -1;
+  }();
+  return v;
 }
 
 // Tile shape per layer.  Every shape uses the same k-tile and MFMA, so the
 // choice never changes a result bit.
 template <int LD>
 hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
-  const long t256 = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
-  if (a.N <= 64) {
-    if ((long)(a.M + 255) / 256 >= 512) return launch_pipe_cfg<256, 64, 3, LD>(a, s);
-    return launch_pipe_cfg<128, 64, 3, LD>(a, s);
+  switch (forced_cfg()) {
+    case 0: return launch_pipe_cfg<256, 128, 2, 2, 3, LD>(a, s);
+    case 1: return launch_pipe_cfg<256, 128, 2, 2, 3, LD, 1>(a, s);
+    case 2: return launch_pipe_cfg<256, 128, 4, 2, 3, LD>(a, s);
+    case 3: return launch_pipe_cfg<128, 64, 2, 2, 3, LD>(a, s);
+    case 4: return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1>(a, s);
+    case 5: return launch_pipe_cfg<256, 128, 2, 2, 2, LD, 1>(a, s);
+    case 6: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1>(a, s);
+    case 7: return launch_pipe_cfg<256, 128, 4, 2, 3, LD, 1>(a, s);
+    case 8: return launch_pipe_cfg<128, 128, 2, 2, 3, LD, 1>(a, s);
+    case 9: return launch_pipe_cfg<256, 64, 4, 1, 3, LD, 1>(a, s);
+    default: break;
   }
-  if (t256 >= 512) return launch_pipe_cfg<256, 128, 3, LD>(a, s);
-  return launch_pipe_cfg<128, 128, 3, LD>(a, s);
+  // Measured on MI355X over the ResNet-50 conv shapes: two workgroups per CU
+  // (74 / 68 KB of LDS) beat larger single-workgroup tiles for every shape.
+  if (a.N <= 64) return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1>(a, s);
+  return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1>(a, s);
 }
 
 template <int LD>
@@ -656,6 +737,9 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
     case LD_NCHW_PATCH:
       return (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) ? launch_pipe_ld<LD_NCHW_PATCH>(a, s)
                                                                  : launch_bf16_ld<LD_NCHW_PATCH>(a, s);
+    case LD_S2D:
+      if (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) return launch_pipe_ld<LD_S2D>(a, s);
+      break;
   }
   return hipErrorInvalidValue;
 }

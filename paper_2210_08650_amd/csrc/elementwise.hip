@@ -272,7 +272,7 @@ template <typename T>
 __global__ void pack_conv_kernel(const float *__restrict__ w, const float *__restrict__ cb,
                                  const float *__restrict__ gamma, const float *__restrict__ beta,
                                  const float *__restrict__ mean, const float *__restrict__ var,
-                                 int N, int C, int kh, int kw, int Kp, int nchw_order,
+                                 int N, int C, int kh, int kw, int Kp, int order,
                                  T *__restrict__ wp, float *__restrict__ bias_out) {
   const int64_t total = (int64_t)N * Kp;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -281,9 +281,16 @@ __global__ void pack_conv_kernel(const float *__restrict__ w, const float *__res
   const int K = C * kh * kw;
   const float sc = gamma ? gamma[n] / sqrtf(var[n] + 1e-5f) : 1.0f;
   float val = 0.0f;
-  if (k < K) {
+  if (order == PACK_S2D) {
+    // k = (du, dv, a, b, c4) over kh2 x kw2 cells: tap (u, v) = (2 du + a, 2 dv + b)
+    const int kw2 = (kw + 1) / 2;
+    const int c = k & 3, b = (k >> 2) & 1, a = (k >> 3) & 1;
+    const int cell = k >> 4, du = cell / kw2, dv = cell % kw2;
+    const int u = 2 * du + a, v = 2 * dv + b;
+    if (c < C && u < kh && v < kw) val = w[(((int64_t)n * C + c) * kh + u) * kw + v] * sc;
+  } else if (k < K) {
     int c, u, v;
-    if (nchw_order) {
+    if (order == PACK_CKHKW) {
       c = k / (kh * kw);
       const int r = k % (kh * kw);
       u = r / kw; v = r % kw;
@@ -301,7 +308,41 @@ __global__ void pack_conv_kernel(const float *__restrict__ w, const float *__res
   }
 }
 
+// Space-to-depth: one thread per output cell, writing its 16 channels (32 B).
+__global__ void s2d_kernel(const uint16_t *__restrict__ x, uint16_t *__restrict__ y, int n, int C,
+                           int H, int W, int pad, int HP, int WP) {
+  const int64_t total = (int64_t)n * HP * WP;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int Q = (int)(i % WP);
+  const int64_t r = i / WP;
+  const int P = (int)(r % HP);
+  const int img = (int)(r / HP);
+  uint16_t v[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int c = q & 3, b = (q >> 2) & 1, a = (q >> 3) & 1;
+    const int h = 2 * P + a - pad, w = 2 * Q + b - pad;
+    v[q] = (c < C && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
+               ? x[(((int64_t)img * C + c) * H + h) * W + w]
+               : (uint16_t)0;
+  }
+  uint4 *dst = reinterpret_cast<uint4 *>(y + i * 16);
+  dst[0] = make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
+                      v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
+  dst[1] = make_uint4(v[8] | ((uint32_t)v[9] << 16), v[10] | ((uint32_t)v[11] << 16),
+                      v[12] | ((uint32_t)v[13] << 16), v[14] | ((uint32_t)v[15] << 16));
+}
+
 }  // namespace
+
+hipError_t launch_space_to_depth(const void *x, void *y, int n, int C, int H, int W, int pad,
+                                 int HP, int WP, hipStream_t s) {
+  const int64_t total = (int64_t)n * HP * WP;
+  hipLaunchKernelGGL(s2d_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+                     (const uint16_t *)x, (uint16_t *)y, n, C, H, W, pad, HP, WP);
+  return hipGetLastError();
+}
 
 hipError_t launch_maxpool(bool bf16, const void *x, void *y, int n, int H, int W, int C, int k,
                           int stride, int pad, int Ho, int Wo, hipStream_t s) {
@@ -397,16 +438,16 @@ hipError_t launch_layernorm(const void *x, const float *gamma, const float *beta
 
 hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, const float *gamma,
                             const float *beta, const float *mean, const float *var, int N, int C,
-                            int kh, int kw, int Kp, bool nchw_order, void *wp, float *bias_out,
+                            int kh, int kw, int Kp, PackOrder order, void *wp, float *bias_out,
                             hipStream_t s) {
   const int64_t total = (int64_t)N * Kp;
   if (bf16)
     hipLaunchKernelGGL(pack_conv_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, Kp, (int)nchw_order,
+                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, Kp, (int)order,
                        (uint16_t *)wp, bias_out);
   else
     hipLaunchKernelGGL(pack_conv_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, Kp, (int)nchw_order,
+                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, Kp, (int)order,
                        (float *)wp, bias_out);
   return hipGetLastError();
 }

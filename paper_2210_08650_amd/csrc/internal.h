@@ -16,7 +16,16 @@ enum Loader : int {
   LD_NHWC = 0,       // NHWC activation, cin % 64 == 0 (bf16) / cin % 16 == 0 (f32)
   LD_GEMM = 1,       // row-major [M, K] matrix: a 1x1 / stride 1 / pad 0 convolution
   LD_NCHW = 2,       // NCHW images, any geometry, element gather (first layer)
-  LD_NCHW_PATCH = 3  // NCHW images, non-overlapping patches with k % 8 == 0 (bf16)
+  LD_NCHW_PATCH = 3, // NCHW images, non-overlapping patches with k % 8 == 0 (bf16)
+  LD_S2D = 4         // space-to-depth cells (see launch_space_to_depth): every k-tile
+                     // is one contiguous 64-element run, zero border, no bounds checks
+};
+
+// Weight order of a packed convolution.
+enum PackOrder : int {
+  PACK_KHKWC = 0,  // k = (kh, kw, c)       NHWC inputs
+  PACK_CKHKW = 1,  // k = (c, kh, kw)       NCHW inputs
+  PACK_S2D = 2     // k = (du, dv, a, b, c4) stride-2 convolution on 2x2 cells
 };
 
 // One convolution / linear layer as an implicit GEMM:
@@ -59,11 +68,17 @@ hipError_t launch_layernorm(const void *x, const float *gamma, const float *beta
                             int64_t rows, int D, float eps, hipStream_t s);
 hipError_t launch_attention(const void *qkv, void *out, int n, int T, int D, int heads,
                             hipStream_t s);
-// Weight packing.  nchw_order: k = (c, kh, kw), else k = (kh, kw, c).
+// Weight packing in the given k order (see PackOrder).
 hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, const float *gamma,
                             const float *beta, const float *mean, const float *var, int N, int C,
-                            int kh, int kw, int Kp, bool nchw_order, void *wp, float *bias_out,
+                            int kh, int kw, int Kp, PackOrder order, void *wp, float *bias_out,
                             hipStream_t s);
+// Space-to-depth for a stride-2 convolution with C <= 4 input channels:
+// y[n][P][Q][(a*2 + b)*4 + c] = x[n][c][2P + a - pad][2Q + b - pad] (0 outside
+// the image or for c >= C), P < HP, Q < WP.  bf16 only.
+hipError_t launch_space_to_depth(const void *x, void *y, int n, int C, int H, int W, int pad,
+                                 int HP, int WP, hipStream_t s);
+constexpr int kS2DChannels = 16;
 hipError_t launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s);
 
 constexpr int kAttnMaxTokens = 256;
