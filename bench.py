@@ -35,6 +35,21 @@ def _cores():
     return min(n, int(omp)) if omp and omp.isdigit() else n
 
 
+def measured_traffic(workload):
+    """HBM bytes per convolution launch from the committed rocprofv3 counter
+    summary, or None when the convolution source changed since it was taken."""
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(root, "profiles", "conv_bf16_resnet50_b256_hbm_traffic.md")
+    if workload != "resnet50_bf16_b256" or not os.path.exists(path):
+        return None
+    kv = dict(line.strip().split("=", 1) for line in open(path) if "=" in line and " " not in line.strip())
+    src = os.path.join(root, "paper_2210_08650_amd", "csrc", "conv.hip")
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != kv.get("conv_source_sha256"):
+        return None
+    return float(kv["conv_traffic_bytes_per_launch"])
+
+
 def cpu_baseline(cfg, budget_s=15.0):
     """The oracle on a bounded sample of the same workload (images/sec)."""
     import synth
@@ -163,7 +178,10 @@ def main():
                    "partitions": H.hapi_chunk_count(desc, B)},
         "mfma_util_pct": mfma_util,
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4),
+                     "traffic": None if args.calib_copy or args.batch else measured_traffic(args.workload),
+                     "algorithmic_bytes_per_launch": round(dom["bytes"] / dom["launches"]),
+                     "algorithmic_flops_per_launch": round(dom["flops"] / dom["launches"]),
                      "kernel": dom["name"], "launches_per_step": dom["launches"] // args.steps,
                      "avg_launch_us": round(dom["total_ms"] * 1e3 / dom["launches"], 2),
                      "share_of_kernel_time": round(dom["total_ms"] / total_kernel_ms, 4)},
