@@ -159,8 +159,11 @@ def main():
         peak = PEAK[cfg["dtype_name"]]
     mfma_util = None if args.calib_copy else round(100.0 * achieved / peak, 2)
 
+    default = args.workload == "resnet50_bf16_b256" and not args.batch and not args.calib_copy
     result = {
-        "metric": "feature-extraction images/sec to split layer (ResNet-50 bf16 b=256); MFMA util %",
+        "metric": ("feature-extraction images/sec to split layer (ResNet-50 bf16 b=256); MFMA util %"
+                   if default else f"feature-extraction images/sec to split layer ({args.workload}, "
+                                   f"batch {B})"),
         "value": round(B * args.steps / elapsed, 2),
         "unit": "images/s",
         "n_gpus": 1,

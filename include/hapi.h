@@ -79,6 +79,11 @@ typedef enum { HAPI_F32 = 0, HAPI_BF16 = 1 } hapi_dtype;
  *                  x += out_proj(MHA(LN1(x))); x += fc2(GELU(fc1(LN2(x)))),
  *                  layernorm eps 1e-6, exact-erf GELU, softmax(QK^T/sqrt(D/heads))V.
  * HAPI_LAYERNORM   cout (= D): per-token layernorm with affine, eps 1e-6.
+ * HAPI_DENSE_BLOCK cin, cout (= cin + n * growth), width (= growth), mlp_dim
+ *                  (= bottleneck channels): DenseNet dense block of n layers;
+ *                  layer l maps the c = cin + l * growth channels so far to
+ *                  conv3x3(ReLU(BN2(conv1x1(ReLU(BN1(x)))))) (growth channels,
+ *                  pad 1) and concatenates them after the existing channels.
  *
  * Batch-norm is inference-mode with eps 1e-5. */
 typedef enum {
@@ -90,7 +95,8 @@ typedef enum {
   HAPI_PATCH_EMBED = 5,
   HAPI_TOKENS = 6,
   HAPI_VIT_BLOCK = 7,
-  HAPI_LAYERNORM = 8
+  HAPI_LAYERNORM = 8,
+  HAPI_DENSE_BLOCK = 9
 } hapi_kind;
 
 typedef struct {
@@ -129,6 +135,9 @@ typedef struct {
  *                value), bias [3D]; out-proj weight [D, D], bias [D]; ln2 gamma,
  *                beta [D]; fc1 weight [mlp, D], bias [mlp]; fc2 weight [D, mlp], bias [D]
  *   LAYERNORM    gamma, beta [D]
+ *   DENSE_BLOCK  per dense layer l (c = cin + l * growth): bn1 gamma, beta, mean,
+ *                var [c]; conv1 weight [bottleneck, c, 1, 1]; bn2 gamma, beta,
+ *                mean, var [bottleneck]; conv2 weight [growth, bottleneck, 3, 3]
  * Returns the number of float32 values, or a negative hapi_status. */
 int64_t hapi_raw_weight_count(const hapi_model_desc *desc);
 

@@ -22,6 +22,9 @@ Parameters follow one canonical order per layer (the raw-weight layout):
                  out-projection weight [D, D], bias [D]; ln2 gamma, beta;
                  fc1 weight [F, D], bias [F]; fc2 weight [D, F], bias [D]
   layernorm      gamma [D], beta [D]
+  dense block    per dense layer l (input channels c = cin + l * growth):
+                 bn1 gamma, beta, mean, var [c]; conv1 weight [bottleneck, c, 1, 1];
+                 bn2 gamma, beta, mean, var [bottleneck]; conv2 weight [growth, bottleneck, 3, 3]
 Convolutions in blocks carry no bias; batch-norm eps is 1e-5, layernorm eps 1e-6.
 """
 from __future__ import annotations
@@ -142,6 +145,41 @@ class Bottleneck:
         y = self.c3.forward(self.c2.forward(self.c1.forward(x, p), p), p)
         r = self.sc.forward(x, p) if self.sc else x
         return L.relu(L.add(y, r))
+
+
+class DenseBlock:
+    """DenseNet dense block: each layer appends growth channels computed from
+    all channels so far, x <- concat(x, conv3x3(ReLU(BN2(conv1x1(ReLU(BN1(x))))))),
+    with pre-activation batch-norm (BN1 acts on the concatenated input)."""
+
+    def __init__(self, cin, n_layers, growth, bottleneck):
+        self.cin, self.n, self.growth, self.bottleneck = cin, n_layers, growth, bottleneck
+
+    def manifest(self):
+        m = []
+        for l in range(self.n):
+            c = self.cin + l * self.growth
+            m += _bn_manifest(c) + [((self.bottleneck, c, 1, 1), "he")]
+            m += _bn_manifest(self.bottleneck) + [((self.growth, self.bottleneck, 3, 3), "he")]
+        return m
+
+    def out_shape(self, s):
+        c, h, w = s
+        assert c == self.cin
+        return (self.cin + self.n * self.growth, h, w)
+
+    def forward(self, x, p):
+        feats = np.asarray(x, np.float64)
+        for _ in range(self.n):
+            g1, b1, m1, v1 = next(p), next(p), next(p), next(p)
+            w1 = next(p)
+            g2, b2, m2, v2 = next(p), next(p), next(p), next(p)
+            w2 = next(p)
+            h = L.relu(L.batchnorm(feats, g1, b1, m1, v1, BN_EPS))
+            t = L.relu(L.batchnorm(L.conv2d(h, w1, None, 1, 0), g2, b2, m2, v2, BN_EPS))
+            new = L.conv2d(t, w2, None, 1, 1)
+            feats = np.concatenate([feats, new], axis=1)
+        return feats
 
 
 class PatchEmbed:
@@ -325,6 +363,13 @@ def resnet50(in_hw=224):
     return _resnet("resnet50", Bottleneck, (3, 4, 6, 3), in_hw)
 
 
+def dense_block_net(in_hw=224, n_layers=4, growth=32, bottleneck=128):
+    """DenseNet-121 stem (conv 7x7/2 + BN + ReLU, maxpool 3x3/2) and one dense
+    block of n_layers at 56 x 56."""
+    return Model("densenet_block", [Conv(3, 64, 7, 2, 3, bn=True), MaxPool(3, 2, 1),
+                                    DenseBlock(64, n_layers, growth, bottleneck)], (3, in_hw, in_hw))
+
+
 def vit(image=224, patch=16, dim=768, heads=12, mlp=3072, depth=12, name="vit_b16"):
     """Vision Transformer encoder: patch embed, tokens, ``depth`` blocks, final LN."""
     g = image // patch
@@ -348,7 +393,7 @@ WORKLOADS = {
 }
 
 FACTORIES = {"alexnet": alexnet, "resnet18": resnet18, "resnet50": resnet50,
-             "vgg16": vgg16, "vit_b16": vit_b16}
+             "vgg16": vgg16, "vit_b16": vit_b16, "densenet_block": dense_block_net}
 
 
 def build(name):

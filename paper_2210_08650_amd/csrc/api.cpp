@@ -60,8 +60,10 @@ struct ConvSpec {
   int64_t pk_w, pk_b;            // byte offsets into the packed buffer
 };
 
-struct Extra {  // float32 parameter copied verbatim (tokens, layernorm)
+struct Extra {  // float32 parameters: copied verbatim (tokens, layernorm), or an
+               // inference batch-norm [g|b|m|v] packed as scale[n], shift[n]
   int64_t raw, pk, n;
+  bool bn_affine;
 };
 
 struct LayerPlan {
@@ -116,9 +118,14 @@ int analyze(const hapi_model_desc *d, Model &m) {
     lp.convs.push_back(c);
   };
   auto add_extra = [&](LayerPlan &lp, int64_t n) {
-    lp.extras.push_back(Extra{raw, pk, n});
+    lp.extras.push_back(Extra{raw, pk, n, false});
     raw += n;
     pk = align_up(pk + n * 4);
+  };
+  auto add_bn_affine = [&](LayerPlan &lp, int64_t c) {
+    lp.extras.push_back(Extra{raw, pk, c, true});
+    raw += 4 * c;
+    pk = align_up(pk + 2 * c * 4);
   };
   // NHWC-input convolutions need whole 16-byte chunks of channels per k-tile.
   auto nhwc_ok = [&](int cin) { return cin % kq == 0; };
@@ -257,6 +264,25 @@ int analyze(const hapi_model_desc *d, Model &m) {
         lp.out = cur;
         break;
       }
+      case HAPI_DENSE_BLOCK: {
+        if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: DENSE_BLOCK needs bf16", li + 1);
+        if (cur.tok || L.cin != cur.c) return fail(HAPI_E_INVAL, "layer %d: DENSE_BLOCK input mismatch", li + 1);
+        const int growth = L.width, bott = L.mlp_dim;
+        if (growth < 1 || bott < 1 || L.cout <= L.cin || (L.cout - L.cin) % growth != 0)
+          return fail(HAPI_E_INVAL, "layer %d: bad dense block (cin %d, cout %d, growth %d)", li + 1,
+                      L.cin, L.cout, growth);
+        if (L.cin % 8 != 0 || growth % 8 != 0 || bott % 64 != 0)
+          return fail(HAPI_E_UNSUPPORTED,
+                      "layer %d: dense block needs cin, growth %% 8 == 0 and bottleneck %% 64 == 0", li + 1);
+        for (int c = L.cin; c < L.cout; c += growth) {
+          add_bn_affine(lp, c);
+          add_conv(lp, c, bott, 1, 1, 0, false, true);
+          add_conv(lp, bott, growth, 3, 1, 1, false, false);
+        }
+        lp.out = Act{L.cout, cur.h, cur.w, false};
+        lp.tmp_elems = (int64_t)std::max(L.cout, bott) * cur.h * cur.w;
+        break;
+      }
       default:
         return fail(HAPI_E_INVAL, "layer %d: unknown kind %d", li + 1, L.kind);
     }
@@ -300,9 +326,9 @@ int64_t workspace_for(const Model &m, int split, int chunk, bool profile, int ba
 // ------------------------------------------------------------- kernel stats
 
 enum Family { F_CONV_BF16, F_CONV_F32, F_ATTN, F_LN, F_MAXPOOL, F_AVGPOOL, F_TOKENS, F_LAYOUT,
-              F_COPY, F_COUNT };
+              F_COPY, F_AFFINE, F_COUNT };
 const char *kFamily[F_COUNT] = {"conv_bf16", "conv_f32", "attention", "layernorm", "maxpool",
-                                "avgpool", "tokens", "layout", "copy"};
+                                "avgpool", "tokens", "layout", "copy", "affine_relu"};
 
 struct StatRec {
   int fam;
@@ -349,7 +375,7 @@ struct Ctx {
 };
 
 hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &in, int nb,
-                    void *y, const void *res, bool relu, bool gelu, bool nchw_input) {
+                    void *y, const void *res, bool relu, bool gelu, bool nchw_input, int ldc = 0) {
   ConvArgs a{};
   a.x = x;
   a.w = c.pk + cs.pk_w;
@@ -369,7 +395,7 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
   a.N = cs.cout;
   a.K = cs.K;
   a.Kp = cs.Kp;
-  a.ldc = cs.cout;
+  a.ldc = ldc ? ldc : cs.cout;
   a.ldr = cs.cout;
   a.relu = relu;
   a.gelu = gelu;
@@ -549,6 +575,36 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
         cur_slot = o;
         break;
       }
+      case HAPI_DENSE_BLOCK: {
+        // Concatenation without copies: the block input is copied once into the
+        // first channels of a buffer with all cout channels, and each dense
+        // layer's 3x3 convolution stores its growth channels into its slice.
+        const int A = free_slot();
+        const int64_t pixels = (int64_t)nb * lp.in.h * lp.in.w;
+        const int cout = L.cout, growth = L.width, bott = L.mlp_dim;
+        uint8_t *cat = c.slot[A];
+        HIP_TRY(timed(c.s, F_COPY, 0.0, 2.0 * pixels * lp.in.c * m.esz, [&] {
+          return launch_channel_copy(cur, cat, pixels, lp.in.c, lp.in.c, cout, 0, c.s);
+        }));
+        const int H = cur_slot, B = free_slot(A);  // block input no longer needed
+        for (size_t l = 0; l < lp.extras.size(); ++l) {
+          const int ch = lp.in.c + (int)l * growth;
+          const Extra &bn = lp.extras[l];
+          HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * ch, 2.0 * pixels * ch * m.esz, [&] {
+            return launch_affine_relu(cat, reinterpret_cast<const float *>(c.pk + bn.pk),
+                                      reinterpret_cast<const float *>(c.pk + bn.pk) + bn.n, c.slot[H],
+                                      pixels, ch, cout, c.s);
+          }));
+          const Act hin{ch, lp.in.h, lp.in.w, false};
+          const Act tin{bott, lp.in.h, lp.in.w, false};
+          HIP_TRY(run_conv(c, lp.convs[2 * l], c.slot[H], hin, nb, c.slot[B], nullptr, true, false, false));
+          HIP_TRY(run_conv(c, lp.convs[2 * l + 1], c.slot[B], tin, nb, cat + (int64_t)ch * m.esz, nullptr,
+                           false, false, false, cout));
+        }
+        cur = cat;
+        cur_slot = A;
+        break;
+      }
       default:
         return fail(HAPI_E_INVAL, "layer %d: unknown kind", li + 1);
     }
@@ -665,8 +721,11 @@ int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void
                                bn ? bn + 3 * c.cout : nullptr, c.cout, c.cin, c.k, c.k, c.Kp, order,
                                pk + c.pk_w, reinterpret_cast<float *>(pk + c.pk_b), s));
     }
-    for (const Extra &e : lp.extras)
-      HIP_TRY(launch_copy_f32(raw + e.raw, reinterpret_cast<float *>(pk + e.pk), e.n, s));
+    for (const Extra &e : lp.extras) {
+      float *dst = reinterpret_cast<float *>(pk + e.pk);
+      if (e.bn_affine) HIP_TRY(launch_pack_affine(raw + e.raw, (int)e.n, dst, dst + e.n, s));
+      else HIP_TRY(launch_copy_f32(raw + e.raw, dst, e.n, s));
+    }
   }
   return HAPI_OK;
 }
@@ -737,7 +796,8 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
       HIP_TRY(launch_fill_pattern(false, pk + c.pk_b, c.cout, 0x77u + (uint32_t)c.pk_b, 0.05f, s));
     }
     for (const Extra &e : lp.extras)
-      HIP_TRY(launch_fill_pattern(false, pk + e.pk, e.n, 0x99u + (uint32_t)e.pk, 0.05f, s));
+      HIP_TRY(launch_fill_pattern(false, pk + e.pk, e.bn_affine ? 2 * e.n : e.n, 0x99u + (uint32_t)e.pk,
+                                  0.05f, s));
   }
   HIP_TRY(launch_fill_pattern(m.bf16, img, (int64_t)batch * m.input.elems(), 0xabcdu, 1.0f, s));
 

@@ -87,8 +87,8 @@ __device__ __forceinline__ uint4 load_a_chunk(const ConvArgs &a, const RowState 
                                               int kh_, int kw_, int c0) {
   const uint16_t *x = static_cast<const uint16_t *>(a.x);
   uint4 v = make_uint4(0, 0, 0, 0);
-  if (LD == LD_GEMM) {
-    if (r.hi0 >= 0) v = *reinterpret_cast<const uint4 *>(x + r.base + k0);
+  if (LD == LD_GEMM) {  // K % 8 == 0; chunks past K read nothing
+    if (r.hi0 >= 0 && k0 < a.K) v = *reinterpret_cast<const uint4 *>(x + r.base + k0);
   } else if (LD == LD_NHWC) {
     const int hi = r.hi0 + kh_, wi = r.wi0 + kw_;
     if ((unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W)
@@ -265,21 +265,26 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int BM, int BN, int STAGES>
+template <int BM, int BN, int STAGES, int EPI>
 struct PipeSmem {
   static constexpr int kStage = (BM + BN) * BK;  // elements per stage
   static constexpr int kCPitch = BN + 4;         // fp32 pitch of the staged C tile
+  static constexpr int kStages = STAGES * kStage * 2;
   static constexpr int kBytes =
-      (STAGES * kStage * 2 > BM * kCPitch * 4) ? STAGES * kStage * 2 : BM * kCPitch * 4;
+      (EPI || kStages > BM * kCPitch * 4) ? kStages : BM * kCPitch * 4;
 };
 
-template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED>
+// EPI = 0: C tile staged through LDS, 16-byte stores.  EPI = 1: MFMA operands
+// swapped (weights as A, activations as B) so each lane's accumulators hold 4
+// consecutive output channels of one output pixel; the epilogue stores them
+// directly as 8-byte writes and the kernel needs no LDS beyond the stages.
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED, int EPI>
 __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a) {
   constexpr int NT = WM * WN * 64;                    // threads: WM x WN waves
   constexpr int TM = BM / (WM * 32), TN = BN / (WN * 32);
   constexpr int NA = BM * 8 / NT, NB = BN * 8 / NT;   // DMA instructions per thread per stage
   constexpr int KS = BK / 16;                         // MFMA k-steps per k-tile
-  using SM = PipeSmem<BM, BN, STAGES>;
+  using SM = PipeSmem<BM, BN, STAGES, EPI>;
   static_assert(TM >= 1 && TN >= 1 && NA >= 1 && NB >= 1, "tile");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
   static_assert((STAGES - 2) * (NA + NB) < 64, "vmcnt range");
@@ -335,8 +340,8 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     for (int i = 0; i < NA; ++i) {
       bool ok;
       int off;
-      if (LD == LD_GEMM) {
-        ok = rhi[i] >= 0;
+      if (LD == LD_GEMM) {  // K % 8 == 0; chunks past K (ragged last k-tile) read zeros
+        ok = rhi[i] >= 0 && kbase + kc8 < a.K;
         off = roff[i] + kbase;
       } else if (LD == LD_NHWC) {
         ok = (unsigned)(rhi[i] + kh_) < (unsigned)a.H && (unsigned)(rwi[i] + kw_) < (unsigned)a.W;
@@ -414,7 +419,8 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = EPI ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0)
+                          : __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
     }
   };
 
@@ -450,6 +456,42 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     __builtin_amdgcn_s_barrier();
     run_tile(smem + (kt % STAGES) * SM::kStage, [] {});
   }
+  if (EPI) {
+    // acc[i][j][4g + e] = C[m][n + e], m = block row + lane % 32,
+    // n = block column + 8 g + 4 (lane / 32).
+    uint16_t *y = static_cast<uint16_t *>(a.y);
+    const uint16_t *res = static_cast<const uint16_t *>(a.res);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = n0 + wn * TN * 32 + j * 32 + 8 * g + 4 * lh;
+        if (n >= a.N) continue;
+        const float4 bv = a.bias ? *reinterpret_cast<const float4 *>(a.bias + n)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int m = m0 + wm * TM * 32 + i * 32 + lrow;
+          if (m >= a.M) continue;
+          float v[4] = {acc[i][j][4 * g] + bv.x, acc[i][j][4 * g + 1] + bv.y,
+                        acc[i][j][4 * g + 2] + bv.z, acc[i][j][4 * g + 3] + bv.w};
+          if (res) {
+            const uint2 rv = *reinterpret_cast<const uint2 *>(res + (int64_t)m * a.ldr + n);
+            v[0] += bf2f((uint16_t)(rv.x & 0xffff));
+            v[1] += bf2f((uint16_t)(rv.x >> 16));
+            v[2] += bf2f((uint16_t)(rv.y & 0xffff));
+            v[3] += bf2f((uint16_t)(rv.y >> 16));
+          }
+          uint2 o;
+          o.x = f2bf(epilogue_act(v[0], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[1], a.relu, a.gelu)) << 16);
+          o.y = f2bf(epilogue_act(v[2], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[3], a.relu, a.gelu)) << 16);
+          *reinterpret_cast<uint2 *>(y + (int64_t)m * a.ldc + n) = o;
+        }
+      }
+    }
+    return;
+  }
+
   // Epilogue: stage the fp32 tile in LDS, then each thread finishes 8
   // consecutive output channels of a row and stores them as one 16-byte write.
   __syncthreads();
@@ -509,10 +551,10 @@ hipError_t launch_bf16_cfg(const ConvArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED = 0>
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED = 1, int EPI = 0>
 hipError_t launch_pipe_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED>), dim3(tiles),
+  hipLaunchKernelGGL((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED, EPI>), dim3(tiles),
                      dim3(WM * WN * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -531,22 +573,29 @@ int forced_cfg() {
 template <int LD>
 hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
   switch (forced_cfg()) {
-    case 0: return launch_pipe_cfg<256, 128, 2, 2, 3, LD>(a, s);
-    case 1: return launch_pipe_cfg<256, 128, 2, 2, 3, LD, 1>(a, s);
-    case 2: return launch_pipe_cfg<256, 128, 4, 2, 3, LD>(a, s);
-    case 3: return launch_pipe_cfg<128, 64, 2, 2, 3, LD>(a, s);
-    case 4: return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1>(a, s);
-    case 5: return launch_pipe_cfg<256, 128, 2, 2, 2, LD, 1>(a, s);
-    case 6: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1>(a, s);
-    case 7: return launch_pipe_cfg<256, 128, 4, 2, 3, LD, 1>(a, s);
-    case 8: return launch_pipe_cfg<128, 128, 2, 2, 3, LD, 1>(a, s);
-    case 9: return launch_pipe_cfg<256, 64, 4, 1, 3, LD, 1>(a, s);
+    case 0: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);
+    case 1: return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1, 0>(a, s);
+    case 2: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 1>(a, s);
+    case 3: return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1, 1>(a, s);
+    case 4: return launch_pipe_cfg<128, 64, 2, 2, 2, LD, 1, 1>(a, s);
+    case 5: return launch_pipe_cfg<256, 128, 4, 2, 2, LD, 1, 1>(a, s);
+    case 6: return launch_pipe_cfg<256, 256, 4, 2, 2, LD, 1, 1>(a, s);
+    case 7: return launch_pipe_cfg<128, 256, 2, 4, 2, LD, 1, 1>(a, s);
+    case 8: return launch_pipe_cfg<256, 128, 2, 2, 2, LD, 1, 1>(a, s);
+    case 9: return launch_pipe_cfg<128, 128, 2, 2, 3, LD, 1, 1>(a, s);
+    case 10: return launch_pipe_cfg<256, 64, 4, 1, 2, LD, 1, 1>(a, s);
+    case 11: return launch_pipe_cfg<64, 128, 1, 4, 3, LD, 1, 1>(a, s);
     default: break;
   }
-  // Measured on MI355X over the ResNet-50 conv shapes: two workgroups per CU
-  // (74 / 68 KB of LDS) beat larger single-workgroup tiles for every shape.
-  if (a.N <= 64) return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1>(a, s);
-  return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1>(a, s);
+  // Measured on MI355X over the ResNet-50 conv shapes: two or three
+  // workgroups per CU beat larger single-workgroup tiles for every shape; the
+  // direct-store epilogue (48 KB of LDS, 3 workgroups per CU) wins only for
+  // 64-channel outputs with long K.
+  if (a.N <= 64) {
+    if (a.K > 256) return launch_pipe_cfg<128, 64, 2, 2, 2, LD, 1, 1>(a, s);
+    return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1, 0>(a, s);
+  }
+  return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);
 }
 
 template <int LD>

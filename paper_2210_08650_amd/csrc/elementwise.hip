@@ -334,7 +334,72 @@ __global__ void s2d_kernel(const uint16_t *__restrict__ x, uint16_t *__restrict_
                       v[12] | ((uint32_t)v[13] << 16), v[14] | ((uint32_t)v[15] << 16));
 }
 
+// Concatenation along channels: one thread per 8 channels (16 bytes).
+__global__ void channel_copy_kernel(const uint16_t *__restrict__ x, uint16_t *__restrict__ y,
+                                    int64_t pixels, int C, int cx, int cy, int off) {
+  const int cg = C / 8;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= pixels * cg) return;
+  const int64_t p = i / cg;
+  const int g = (int)(i % cg);
+  *reinterpret_cast<uint4 *>(y + p * cy + off + g * 8) =
+      *reinterpret_cast<const uint4 *>(x + p * cx + g * 8);
+}
+
+// Pre-activation batch-norm + ReLU on a channel prefix, 8 channels per thread.
+__global__ void affine_relu_kernel(const uint16_t *__restrict__ x, const float *__restrict__ scale,
+                                   const float *__restrict__ shift, uint16_t *__restrict__ y,
+                                   int64_t pixels, int C, int cx) {
+  const int cg = C / 8;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= pixels * cg) return;
+  const int64_t p = i / cg;
+  const int g = (int)(i % cg);
+  const uint4 q = *reinterpret_cast<const uint4 *>(x + p * cx + g * 8);
+  const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = g * 8 + 2 * j;
+    const float lo = fmaxf(bf2f((uint16_t)(w4[j] & 0xffff)) * scale[c] + shift[c], 0.0f);
+    const float hi = fmaxf(bf2f((uint16_t)(w4[j] >> 16)) * scale[c + 1] + shift[c + 1], 0.0f);
+    o[j] = f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+  }
+  *reinterpret_cast<uint4 *>(y + p * C + g * 8) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+__global__ void pack_affine_kernel(const float *__restrict__ bn, int C, float *__restrict__ scale,
+                                   float *__restrict__ shift) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  const float sc = bn[c] / sqrtf(bn[3 * C + c] + 1e-5f);
+  scale[c] = sc;
+  shift[c] = bn[C + c] - bn[2 * C + c] * sc;
+}
+
 }  // namespace
+
+hipError_t launch_channel_copy(const void *x, void *y, int64_t pixels, int C, int cx, int cy,
+                               int off, hipStream_t s) {
+  const int64_t total = pixels * (C / 8);
+  hipLaunchKernelGGL(channel_copy_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+                     (const uint16_t *)x, (uint16_t *)y, pixels, C, cx, cy, off);
+  return hipGetLastError();
+}
+
+hipError_t launch_affine_relu(const void *x, const float *scale, const float *shift, void *y,
+                              int64_t pixels, int C, int cx, hipStream_t s) {
+  const int64_t total = pixels * (C / 8);
+  hipLaunchKernelGGL(affine_relu_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+                     (const uint16_t *)x, scale, shift, (uint16_t *)y, pixels, C, cx);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_affine(const float *bn, int C, float *scale, float *shift, hipStream_t s) {
+  hipLaunchKernelGGL(pack_affine_kernel, dim3(blocks_for(C, 256)), dim3(256), 0, s, bn, C, scale,
+                     shift);
+  return hipGetLastError();
+}
 
 hipError_t launch_space_to_depth(const void *x, void *y, int n, int C, int H, int W, int pad,
                                  int HP, int WP, hipStream_t s) {

@@ -10,8 +10,8 @@ distribution each synthetic stand-in for pre-trained weights is drawn from.
 from __future__ import annotations
 
 from .binding import (HAPI_AVGPOOL, HAPI_BASIC_BLOCK, HAPI_BF16, HAPI_BOTTLENECK, HAPI_CONV,
-                      HAPI_F32, HAPI_LAYERNORM, HAPI_MAXPOOL, HAPI_PATCH_EMBED, HAPI_TOKENS,
-                      HAPI_VIT_BLOCK)
+                      HAPI_DENSE_BLOCK, HAPI_F32, HAPI_LAYERNORM, HAPI_MAXPOOL, HAPI_PATCH_EMBED,
+                      HAPI_TOKENS, HAPI_VIT_BLOCK)
 
 
 def conv(cin, cout, k, stride=1, pad=0, bias=False, bn=False, relu=True):
@@ -71,6 +71,17 @@ def resnet50():
     return _resnet(True, (3, 4, 6, 3))
 
 
+def dense_block(cin, n_layers, growth=32, bottleneck=128):
+    return dict(kind=HAPI_DENSE_BLOCK, cin=cin, cout=cin + n_layers * growth, width=growth,
+                mlp_dim=bottleneck)
+
+
+def dense_block_net(n_layers=4, growth=32, bottleneck=128):
+    """DenseNet-121 stem and one dense block at 56 x 56 (channel concatenation)."""
+    return [conv(3, 64, 7, 2, 3, bn=True), maxpool(3, 2, 1),
+            dense_block(64, n_layers, growth, bottleneck)]
+
+
 def vit(image=224, patch=16, dim=768, heads=12, mlp=3072, depth=12):
     layers = [dict(kind=HAPI_PATCH_EMBED, cin=3, cout=dim, k=patch, stride=patch),
               dict(kind=HAPI_TOKENS, cout=dim)]
@@ -85,7 +96,7 @@ def vit_b16():
 
 
 FACTORIES = {"alexnet": alexnet, "resnet18": resnet18, "resnet50": resnet50,
-             "vgg16": vgg16, "vit_b16": vit_b16}
+             "vgg16": vgg16, "vit_b16": vit_b16, "densenet_block": dense_block_net}
 
 # The five benchmark workloads.  ``seed`` selects the synthetic input stream.
 WORKLOADS = {
@@ -94,6 +105,9 @@ WORKLOADS = {
     "vgg16_bf16_b128": dict(seed=2, model="vgg16", dtype=HAPI_BF16, batch=128, split=18),
     "resnet50_bf16_b256": dict(seed=3, model="resnet50", dtype=HAPI_BF16, batch=256, split=18),
     "vit_b16_bf16_b128": dict(seed=4, model="vit_b16", dtype=HAPI_BF16, batch=128, split=10),
+    # synthetic 4-layer dense block (growth 32, 56 x 56) for the channel-concat path
+    "densenet_block_bf16_b64": dict(seed=5, model="densenet_block", dtype=HAPI_BF16, batch=64,
+                                    split=3),
 }
 
 
@@ -150,6 +164,11 @@ def raw_manifest(layers, in_shape=(3, 224, 224)):
                   ((F, D), "tn02"), ((F,), "tn02"), ((D, F), "tn02"), ((D,), "tn02")]
         elif kind == HAPI_LAYERNORM:
             m += [((L["cout"],), "ln_gamma"), ((L["cout"],), "ln_beta")]
+        elif kind == HAPI_DENSE_BLOCK:
+            g, bt = L["width"], L["mlp_dim"]
+            for ch in range(L["cin"], L["cout"], g):
+                m += _bn(ch) + [((bt, ch, 1, 1), "he")] + _bn(bt) + [((g, bt, 3, 3), "he")]
+            c = L["cout"]
         else:
             raise ValueError(f"unknown layer kind {kind}")
     return m

@@ -31,7 +31,7 @@ def _setup(name, seed, batch, layers=None, omodel=None, in_shape=(3, 224, 224), 
 
 
 @pytest.mark.parametrize("name,batch", [("alexnet", 4), ("resnet18", 3), ("resnet50", 2),
-                                        ("vgg16", 2), ("vit_b16", 2)])
+                                        ("vgg16", 2), ("vit_b16", 2), ("densenet_block", 3)])
 def test_every_split_matches_oracle(name, batch):
     r, om, ps, xd, xv, dtype = _setup(name, 10 + len(name), batch)
     outs = om.forward(ps, xv, om.n_layers, collect=True)
@@ -57,6 +57,28 @@ def test_chunking_is_bit_exact(name, split, chunks):
     # row i depends on image i only
     single = r.extract_np(xd[3:4].contiguous(), split)
     assert np.array_equal(single[0], whole[3])
+
+
+def test_dense_block_concat_keeps_input_bits():
+    # The first cin channels of a dense block's output are its input, copied.
+    r, _, _, xd, _, _ = _setup("densenet_block", 80, 3)
+    before = r.extract_np(xd, 2)
+    after = r.extract_np(xd, 3)
+    assert after.shape == (3, 192, 56, 56)
+    assert np.array_equal(after[:, :64], before)
+
+
+def test_dense_block_ragged_channels():
+    # 40 input channels: the 1x1 convolutions see K = 40, 56, 72 (not multiples
+    # of the 64-wide k-tile) and the concat slices start at 8-channel offsets.
+    layers = [PM.maxpool(1, 1), PM.dense_block(40, 3, growth=16, bottleneck=64)]
+    om = OM.Model("dense_ragged", [OM.MaxPool(1, 1), OM.DenseBlock(40, 3, 16, 64)], (40, 13, 11))
+    r, om, ps, xd, xv, _ = _setup("densenet_block", 81, 2, layers=layers, omodel=om,
+                                  in_shape=(40, 13, 11))
+    got = r.extract_np(xd, 2)
+    ref = om.forward(ps, xv, 2)
+    assert np.array_equal(got[:, :40], xv)
+    assert rel_l2(got, ref) <= 2e-2
 
 
 def _vit_small(depth=2):

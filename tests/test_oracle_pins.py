@@ -394,3 +394,43 @@ def test_split_zero_is_input():
     m = M.alexnet()
     x = synth.images(0, 2)
     assert np.array_equal(m.forward(synth.params(0, m.manifest()), x, 0), x.astype(np.float64))
+
+
+# ----------------------------------------------------------- dense block
+
+def _torch_dense_block(x, params, n, growth):
+    """DenseNet dense layers restated with torch.nn.functional (float64)."""
+    it = iter(params)
+    feats = _t(x)
+    for _ in range(n):
+        g1, b1, m1, v1, w1, g2, b2, m2, v2, w2 = (_t(next(it)) for _ in range(10))
+        h = F.relu(F.batch_norm(feats, m1, v1, g1, b1, training=False, eps=1e-5))
+        t = F.relu(F.batch_norm(F.conv2d(h, w1), m2, v2, g2, b2, training=False, eps=1e-5))
+        feats = torch.cat([feats, F.conv2d(t, w2, padding=1)], 1)
+    return feats.numpy()
+
+
+def test_dense_block_vs_torch_and_concat_prefix():
+    blk = M.DenseBlock(16, 3, 8, 32)
+    ps = synth.params(55, blk.manifest())
+    x = np.random.default_rng(15).standard_normal((2, 16, 9, 9))
+    y = blk.forward(x, iter(ps))
+    assert y.shape == (2, 16 + 3 * 8, 9, 9)
+    np.testing.assert_allclose(y, _torch_dense_block(x, ps, 3, 8), rtol=1e-10, atol=1e-10)
+    # concatenation keeps the block input verbatim in the first channels
+    assert np.array_equal(y[:, :16], x)
+
+
+def test_dense_block_with_zero_growth_convs_appends_zeros():
+    blk = M.DenseBlock(8, 2, 4, 16)
+    ps = synth.params(56, blk.manifest())
+    for i in (9, 19):          # conv2 weights of both layers
+        ps[i] = np.zeros_like(ps[i])
+    x = np.random.default_rng(16).standard_normal((1, 8, 5, 5))
+    y = blk.forward(x, iter(ps))
+    assert np.array_equal(y[:, :8], x) and not y[:, 8:].any()
+
+
+def test_dense_block_net_shapes():
+    m = M.dense_block_net()
+    assert m.shapes() == [(3, 224, 224), (64, 112, 112), (64, 56, 56), (192, 56, 56)]
