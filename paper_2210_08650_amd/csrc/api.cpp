@@ -58,6 +58,12 @@ struct ConvSpec {
   int K, Kp;
   int64_t raw_w, raw_b, raw_bn;  // float offsets into the raw buffer (-1: absent)
   int64_t pk_w, pk_b;            // byte offsets into the packed buffer
+  // A residual block's last convolution fused with its projection shortcut:
+  // one GEMM over K = K1 (this convolution) + cin2 (1x1, stride stride2, on the
+  // block input); both batch-norms folded, biases summed.
+  bool fused;
+  int K1, cin2, stride2;
+  int64_t raw_w2, raw_bn2;
 };
 
 struct Extra {  // float32 parameters: copied verbatim (tokens, layernorm), or an
@@ -113,6 +119,21 @@ int analyze(const hapi_model_desc *d, Model &m) {
     c.raw_b = -1; c.raw_bn = -1;
     if (bias) { c.raw_b = raw; raw += cout; }
     if (bn) { c.raw_bn = raw; raw += 4 * (int64_t)cout; }
+    c.pk_w = pk; pk = align_up(pk + (int64_t)cout * c.Kp * m.esz);
+    c.pk_b = pk; pk = align_up(pk + (int64_t)cout * 4);
+    lp.convs.push_back(c);
+  };
+  auto add_fused = [&](LayerPlan &lp, int cin1, int cout, int k, int pad, int cin2, int s2) {
+    ConvSpec c{};
+    c.cin = cin1; c.cout = cout; c.k = k; c.stride = 1; c.pad = pad; c.bn = true;
+    c.fused = true;
+    c.K1 = cin1 * k * k; c.cin2 = cin2; c.stride2 = s2;
+    c.K = c.Kp = c.K1 + cin2;
+    c.raw_b = -1;
+    c.raw_w = raw; raw += (int64_t)cout * c.K1;
+    c.raw_bn = raw; raw += 4 * (int64_t)cout;
+    c.raw_w2 = raw; raw += (int64_t)cout * cin2;
+    c.raw_bn2 = raw; raw += 4 * (int64_t)cout;
     c.pk_w = pk; pk = align_up(pk + (int64_t)cout * c.Kp * m.esz);
     c.pk_b = pk; pk = align_up(pk + (int64_t)cout * 4);
     lp.convs.push_back(c);
@@ -192,15 +213,21 @@ int analyze(const hapi_model_desc *d, Model &m) {
         const int ho = conv_out(cur.h, 3, L.stride, 1), wo = conv_out(cur.w, 3, L.stride, 1);
         if (ho < 1 || wo < 1) return fail(HAPI_E_INVAL, "layer %d: empty block output", li + 1);
         lp.has_sc = L.stride != 1 || L.cin != cout;
+        // bf16: the projection shortcut joins the last convolution's GEMM when
+        // both K parts are whole 64-wide k-tiles of NHWC channels
+        const bool fuse = lp.has_sc && m.bf16 && L.cin % 64 == 0 &&
+                          (basic ? cout : width) % 64 == 0 && cout % 8 == 0;
         if (basic) {
           add_conv(lp, L.cin, cout, 3, L.stride, 1, false, true);
-          add_conv(lp, cout, cout, 3, 1, 1, false, true);
+          if (fuse) add_fused(lp, cout, cout, 3, 1, L.cin, L.stride);
+          else add_conv(lp, cout, cout, 3, 1, 1, false, true);
         } else {
           add_conv(lp, L.cin, width, 1, 1, 0, false, true);
           add_conv(lp, width, width, 3, L.stride, 1, false, true);
-          add_conv(lp, width, cout, 1, 1, 0, false, true);
+          if (fuse) add_fused(lp, width, cout, 1, 0, L.cin, L.stride);
+          else add_conv(lp, width, cout, 1, 1, 0, false, true);
         }
-        if (lp.has_sc) add_conv(lp, L.cin, cout, 1, L.stride, 0, false, true);
+        if (lp.has_sc && !fuse) add_conv(lp, L.cin, cout, 1, L.stride, 0, false, true);
         lp.out = Act{cout, ho, wo, false};
         lp.tmp_elems = std::max<int64_t>(lp.tmp_elems, (int64_t)width * cur.h * cur.w);
         lp.tmp_elems = std::max<int64_t>(lp.tmp_elems, (int64_t)width * ho * wo);
@@ -375,7 +402,8 @@ struct Ctx {
 };
 
 hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &in, int nb,
-                    void *y, const void *res, bool relu, bool gelu, bool nchw_input, int ldc = 0) {
+                    void *y, const void *res, bool relu, bool gelu, bool nchw_input, int ldc = 0,
+                    const void *x2 = nullptr, const Act *in2 = nullptr) {
   ConvArgs a{};
   a.x = x;
   a.w = c.pk + cs.pk_w;
@@ -400,7 +428,15 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
   a.relu = relu;
   a.gelu = gelu;
   Loader ld;
-  if (cs.s2d) {
+  if (cs.fused) {
+    a.x2 = x2;
+    a.H2 = in2->h;
+    a.W2 = in2->w;
+    a.C2 = in2->c;
+    a.s2 = cs.stride2;
+    a.K1 = cs.K1;
+    ld = LD_CAT;
+  } else if (cs.s2d) {
     // x is the space-to-depth buffer: a stride-1 4 x 4 convolution over cells.
     const int k2 = (cs.k + 1) / 2;
     a.H = a.Ho + k2 - 1;
@@ -419,7 +455,7 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
   }
   const double flops = 2.0 * a.M * (double)a.N * a.K;
   const double bytes = (double)c.m.esz * ((double)nb * in.elems() + (double)a.M * a.N * (res ? 2 : 1) +
-                                          (double)a.N * a.K);
+                                          (double)a.N * a.K + (cs.fused ? (double)a.M * cs.cin2 : 0.0));
   if (c.m.bf16)
     return timed(c.s, F_CONV_BF16, flops, bytes, [&] { return launch_conv_bf16(a, ld, c.s); });
   return timed(c.s, F_CONV_F32, flops, bytes, [&] { return launch_conv_f32(a, ld, c.s); });
@@ -498,6 +534,14 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
         const int A = free_slot();
         const Act mid{lp.out.c, lp.out.h, lp.out.w, false};
         HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
+        if (lp.convs[1].fused) {  // conv2 and the projection shortcut in one GEMM
+          const int B = free_slot(A);
+          HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], mid, nb, c.slot[B], nullptr, true, false, false, 0,
+                           cur, &lp.in));
+          cur = c.slot[B];
+          cur_slot = B;
+          break;
+        }
         const void *res = cur;
         if (lp.has_sc) {
           const int B = free_slot(A);
@@ -517,6 +561,13 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
         const Act a2{width, lp.out.h, lp.out.w, false};
         HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
         HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], a1, nb, c.slot[B], nullptr, true, false, false));
+        if (lp.convs[2].fused) {  // c3 and the projection shortcut in one GEMM, into the free slot
+          HIP_TRY(run_conv(c, lp.convs[2], c.slot[B], a2, nb, c.slot[A], nullptr, true, false, false, 0,
+                           cur, &lp.in));
+          cur = c.slot[A];
+          cur_slot = A;
+          break;
+        }
         const void *res = cur;
         if (lp.has_sc) {
           HIP_TRY(run_conv(c, lp.convs[3], cur, lp.in, nb, c.slot[A], nullptr, false, false, false));
@@ -716,10 +767,17 @@ int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void
     for (const ConvSpec &c : lp.convs) {
       const float *bn = c.raw_bn >= 0 ? raw + c.raw_bn : nullptr;
       const PackOrder order = c.s2d ? PACK_S2D : nchw ? PACK_CKHKW : PACK_KHKWC;
+      float *bias = reinterpret_cast<float *>(pk + c.pk_b);
       HIP_TRY(launch_pack_conv(m.bf16, raw + c.raw_w, c.raw_b >= 0 ? raw + c.raw_b : nullptr,
                                bn, bn ? bn + c.cout : nullptr, bn ? bn + 2 * c.cout : nullptr,
-                               bn ? bn + 3 * c.cout : nullptr, c.cout, c.cin, c.k, c.k, c.Kp, order,
-                               pk + c.pk_w, reinterpret_cast<float *>(pk + c.pk_b), s));
+                               bn ? bn + 3 * c.cout : nullptr, c.cout, c.cin, c.k, c.k,
+                               c.fused ? c.K1 : c.Kp, c.Kp, 0, false, order, pk + c.pk_w, bias, s));
+      if (c.fused) {
+        const float *bn2 = raw + c.raw_bn2;
+        HIP_TRY(launch_pack_conv(m.bf16, raw + c.raw_w2, nullptr, bn2, bn2 + c.cout, bn2 + 2 * c.cout,
+                                 bn2 + 3 * c.cout, c.cout, c.cin2, 1, 1, c.cin2, c.Kp, c.K1, true,
+                                 PACK_KHKWC, pk + c.pk_w, bias, s));
+      }
     }
     for (const Extra &e : lp.extras) {
       float *dst = reinterpret_cast<float *>(pk + e.pk);

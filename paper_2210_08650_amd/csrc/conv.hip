@@ -251,8 +251,10 @@ __global__ __launch_bounds__(kThreads) void conv_bf16_kernel(ConvArgs a) {
 // and rows beyond M / N read a zero chunk in global memory instead.
 //
 // LDS rows hold 64 bf16 (128 B) without padding; the 16-byte chunk kc of row
-// r is stored at position kc ^ (r & 7), so the 32 rows an MFMA fragment read
-// touches in one step spread over all banks.
+// r is stored at position kc ^ ((r >> 1) & 7).  The LDS serves 256 bytes (64
+// banks) per clock, i.e. two 128-byte rows: with this swizzle the 16 rows a
+// quarter-wave fragment read touches land in 16 distinct 16-byte slots of
+// that 256-byte window, so fragment reads are free of bank conflicts.
 
 __device__ __attribute__((aligned(64))) uint4 g_zero_chunk[4];
 
@@ -268,7 +270,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 template <int BM, int BN, int STAGES, int EPI>
 struct PipeSmem {
   static constexpr int kStage = (BM + BN) * BK;  // elements per stage
-  static constexpr int kCPitch = BN + 4;         // fp32 pitch of the staged C tile
+  static constexpr int kCPitch = BN + 8;         // fp32 pitch of the staged C tile
   static constexpr int kStages = STAGES * kStage * 2;
   static constexpr int kBytes =
       (EPI || kStages > BM * kCPitch * 4) ? kStages : BM * kCPitch * 4;
@@ -296,22 +298,39 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int kc8 = ((lane & 7) ^ (lane >> 3)) * 8;  // first k of the chunk this lane moves
+  // Lane l of DMA instruction q (q = wave * NA + i, 8 rows of 8 chunks) fills
+  // row 8 q + l / 8, physical chunk l % 8, i.e. logical chunk
+  // (l % 8) ^ ((row >> 1) & 7) = (l % 8) ^ ((4 q + l / 16) & 7).
+  const int kcA = ((lane & 7) ^ ((lane >> 4) & 7)) * 8;        // even q
+  const int kcB = ((lane & 7) ^ ((4 + (lane >> 4)) & 7)) * 8;  // odd q
   const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero_chunk);
   const uint16_t *x = static_cast<const uint16_t *>(a.x);
   const uint16_t *wp = static_cast<const uint16_t *>(a.w);
 
   // Per-row gather state, computed once: element offset of the row's first
   // tap (may point into padding), and the tap origin for bounds checks.
-  int roff[NA], rhi[NA], rwi[NA];
+  int roff[NA], rhi[NA], rwi[NA], rkc[NA], roff2[LD == LD_CAT ? NA : 1];
+  const uint16_t *x2 = static_cast<const uint16_t *>(a.x2);
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
-    const RowState r = make_row<LD>(a, m0 + (wave * NA + i) * 8 + (lane >> 3));
+    const int m = m0 + (wave * NA + i) * 8 + (lane >> 3);
+    const RowState r = make_row<LD == LD_CAT ? LD_NHWC : LD>(a, m);
+    const int kc8 = ((wave * NA + i) & 1) ? kcB : kcA;
+    rkc[i] = kc8;
     rhi[i] = r.hi0;
     rwi[i] = r.wi0;
-    if (LD == LD_NHWC || LD == LD_S2D) roff[i] = r.base + (r.hi0 * a.W + r.wi0) * a.C + kc8;
+    if (LD == LD_NHWC || LD == LD_S2D || LD == LD_CAT)
+      roff[i] = r.base + (r.hi0 * a.W + r.wi0) * a.C + kc8;
     else if (LD == LD_GEMM) roff[i] = r.base + kc8;
     else roff[i] = r.base;
+    if (LD == LD_CAT) {
+      // shortcut pixel (n, ho * s2, wo * s2) of x2
+      const int hw = a.Ho * a.Wo;
+      const int mm = m < a.M ? m : 0;
+      const int n = mm / hw, rem = mm - n * hw;
+      const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
+      roff2[i] = ((n * a.H2 + ho * a.s2) * a.W2 + wo * a.s2) * a.C2 + kc8 - a.K1;
+    }
   }
   int boffs[NB];
   bool bok[NB];
@@ -319,7 +338,7 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   for (int j = 0; j < NB; ++j) {
     const int n = n0 + (wave * NB + j) * 8 + (lane >> 3);
     bok[j] = n < a.N;
-    boffs[j] = (bok[j] ? n : 0) * a.Kp + kc8;
+    boffs[j] = (bok[j] ? n : 0) * a.Kp + (((wave * NB + j) & 1) ? kcB : kcA);
   }
   const int nk = a.Kp / BK;
 
@@ -330,18 +349,19 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     uint16_t *Bs = As + BM * BK;
     const int kbase = kt * BK;
     int kh_ = 0, kw_ = 0, tapoff = 0;
-    if (LD == LD_NHWC) {
+    if (LD == LD_NHWC || LD == LD_CAT) {
       const int tap = kbase / a.C;
       kh_ = tap / a.kw;
       kw_ = tap - kh_ * a.kw;
       tapoff = (kh_ * a.W + kw_) * a.C + (kbase - tap * a.C);
     }
+    const uint16_t *xs = (LD == LD_CAT && kbase >= a.K1) ? x2 : x;
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       bool ok;
       int off;
       if (LD == LD_GEMM) {  // K % 8 == 0; chunks past K (ragged last k-tile) read zeros
-        ok = rhi[i] >= 0 && kbase + kc8 < a.K;
+        ok = rhi[i] >= 0 && kbase + rkc[i] < a.K;
         off = roff[i] + kbase;
       } else if (LD == LD_NHWC) {
         ok = (unsigned)(rhi[i] + kh_) < (unsigned)a.H && (unsigned)(rwi[i] + kw_) < (unsigned)a.W;
@@ -350,15 +370,23 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
         // k-tile kt is the contiguous run of cell row du = kt (kw x 16 = 64 elements)
         ok = rhi[i] >= 0;
         off = roff[i] + kt * a.W * a.C;
+      } else if (LD == LD_CAT) {
+        if (kbase < a.K1) {
+          ok = (unsigned)(rhi[i] + kh_) < (unsigned)a.H && (unsigned)(rwi[i] + kw_) < (unsigned)a.W;
+          off = roff[i] + tapoff;
+        } else {
+          ok = rhi[i] > -(1 << 27);
+          off = roff2[i] + kbase;
+        }
       } else {  // LD_NCHW_PATCH: k = (c, u, v), 8 | kw
-        const int k0 = kbase + kc8;
+        const int k0 = kbase + rkc[i];
         const int khw = a.kh * a.kw;
         const int c = k0 / khw, rem = k0 - c * khw;
         const int u = rem / a.kw, vv = rem - u * a.kw;
         ok = rhi[i] > -(1 << 27) && k0 < a.K;
         off = roff[i] + (c * a.H + rhi[i] + u) * a.W + rwi[i] + vv;
       }
-      const uint16_t *src = ok ? x + off : zero;
+      const uint16_t *src = ok ? xs + off : zero;
       __builtin_amdgcn_global_load_lds(src, LDS_PTR(As + (wave * NA + i) * 512), 16, 0, 0);
     }
 #pragma unroll
@@ -371,13 +399,14 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   const int wm = wave / WN, wn = wave % WN;
   const int lrow = lane & 31, lh = lane >> 5;
   // Fragment offsets inside a stage; k-step ks reads logical chunk 2 ks + lh,
-  // stored at physical chunk (2 ks + lh) ^ (row & 7), and row & 7 == lrow & 7.
+  // stored at physical chunk (2 ks + lh) ^ ((row >> 1) & 7), and fragment rows
+  // are 32-aligned, so (row >> 1) & 7 == (lrow >> 1) & 7.
   int aoff[TM], boff[TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i) aoff[i] = (wm * TM * 32 + i * 32 + lrow) * BK;
 #pragma unroll
   for (int j = 0; j < TN; ++j) boff[j] = BM * BK + (wn * TN * 32 + j * 32 + lrow) * BK;
-  const int sw = lrow & 7;
+  const int sw = (lrow >> 1) & 7;
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -788,6 +817,9 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
                                                                  : launch_bf16_ld<LD_NCHW_PATCH>(a, s);
     case LD_S2D:
       if (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) return launch_pipe_ld<LD_S2D>(a, s);
+      break;
+    case LD_CAT:
+      if (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) return launch_pipe_ld<LD_CAT>(a, s);
       break;
   }
   return hipErrorInvalidValue;

@@ -272,12 +272,13 @@ template <typename T>
 __global__ void pack_conv_kernel(const float *__restrict__ w, const float *__restrict__ cb,
                                  const float *__restrict__ gamma, const float *__restrict__ beta,
                                  const float *__restrict__ mean, const float *__restrict__ var,
-                                 int N, int C, int kh, int kw, int Kp, int order,
-                                 T *__restrict__ wp, float *__restrict__ bias_out) {
-  const int64_t total = (int64_t)N * Kp;
+                                 int N, int C, int kh, int kw, int kcols, int ldw, int koff,
+                                 int acc_bias, int order, T *__restrict__ wp,
+                                 float *__restrict__ bias_out) {
+  const int64_t total = (int64_t)N * kcols;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= total) return;
-  const int n = (int)(i / Kp), k = (int)(i % Kp);
+  const int n = (int)(i / kcols), k = (int)(i % kcols);
   const int K = C * kh * kw;
   const float sc = gamma ? gamma[n] / sqrtf(var[n] + 1e-5f) : 1.0f;
   float val = 0.0f;
@@ -301,10 +302,11 @@ __global__ void pack_conv_kernel(const float *__restrict__ w, const float *__res
     }
     val = w[(((int64_t)n * C + c) * kh + u) * kw + v] * sc;
   }
-  Elt<T>::st(wp, i, val);
+  Elt<T>::st(wp, (int64_t)n * ldw + koff + k, val);
   if (k == 0) {
     const float b = cb ? cb[n] : 0.0f;
-    bias_out[n] = gamma ? (b - mean[n]) * sc + beta[n] : b;
+    const float folded = gamma ? (b - mean[n]) * sc + beta[n] : b;
+    bias_out[n] = acc_bias ? bias_out[n] + folded : folded;
   }
 }
 
@@ -503,17 +505,17 @@ hipError_t launch_layernorm(const void *x, const float *gamma, const float *beta
 
 hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, const float *gamma,
                             const float *beta, const float *mean, const float *var, int N, int C,
-                            int kh, int kw, int Kp, PackOrder order, void *wp, float *bias_out,
-                            hipStream_t s) {
-  const int64_t total = (int64_t)N * Kp;
+                            int kh, int kw, int kcols, int ldw, int koff, bool acc_bias,
+                            PackOrder order, void *wp, float *bias_out, hipStream_t s) {
+  const int64_t total = (int64_t)N * kcols;
   if (bf16)
     hipLaunchKernelGGL(pack_conv_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, Kp, (int)order,
-                       (uint16_t *)wp, bias_out);
+                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, kcols, ldw, koff,
+                       (int)acc_bias, (int)order, (uint16_t *)wp, bias_out);
   else
     hipLaunchKernelGGL(pack_conv_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, Kp, (int)order,
-                       (float *)wp, bias_out);
+                       w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, kcols, ldw, koff,
+                       (int)acc_bias, (int)order, (float *)wp, bias_out);
   return hipGetLastError();
 }
 

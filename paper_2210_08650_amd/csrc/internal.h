@@ -17,8 +17,10 @@ enum Loader : int {
   LD_GEMM = 1,       // row-major [M, K] matrix: a 1x1 / stride 1 / pad 0 convolution
   LD_NCHW = 2,       // NCHW images, any geometry, element gather (first layer)
   LD_NCHW_PATCH = 3, // NCHW images, non-overlapping patches with k % 8 == 0 (bf16)
-  LD_S2D = 4         // space-to-depth cells (see launch_space_to_depth): every k-tile
+  LD_S2D = 4,        // space-to-depth cells (see launch_space_to_depth): every k-tile
                      // is one contiguous 64-element run, zero border, no bounds checks
+  LD_CAT = 5         // two sources along K: k < K1 as LD_NHWC over x, k >= K1 a 1x1
+                     // convolution with stride s2 over x2 (a residual block's shortcut)
 };
 
 // Weight order of a packed convolution.
@@ -44,6 +46,9 @@ struct ConvArgs {
   int M, N, K, Kp;
   int ldc, ldr;
   int relu, gelu;
+  // LD_CAT only: second source [n, H2, W2, C2] NHWC, read at stride s2; K1 = % 64
+  const void *x2;
+  int H2, W2, C2, s2, K1;
 };
 
 hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s);
@@ -68,11 +73,14 @@ hipError_t launch_layernorm(const void *x, const float *gamma, const float *beta
                             int64_t rows, int D, float eps, hipStream_t s);
 hipError_t launch_attention(const void *qkv, void *out, int n, int T, int D, int heads,
                             hipStream_t s);
-// Weight packing in the given k order (see PackOrder).
+// Weight packing in the given k order (see PackOrder): writes columns
+// [koff, koff + kcols) of rows n < N with row pitch ldw (columns past the
+// weight's own K are zero), and the folded bias (added to bias_out when
+// acc_bias, else stored).
 hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, const float *gamma,
                             const float *beta, const float *mean, const float *var, int N, int C,
-                            int kh, int kw, int Kp, PackOrder order, void *wp, float *bias_out,
-                            hipStream_t s);
+                            int kh, int kw, int kcols, int ldw, int koff, bool acc_bias,
+                            PackOrder order, void *wp, float *bias_out, hipStream_t s);
 // Space-to-depth for a stride-2 convolution with C <= 4 input channels:
 // y[n][P][Q][(a*2 + b)*4 + c] = x[n][c][2P + a - pad][2Q + b - pad] (0 outside
 // the image or for c >= C), P < HP, Q < WP.  bf16 only.
