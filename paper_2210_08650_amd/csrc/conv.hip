@@ -16,6 +16,9 @@
 // of M.  Results are therefore bit-identical for any batch split.
 #include <cstdlib>
 
+#include <type_traits>
+#include <utility>
+
 #include "internal.h"
 
 namespace hapi {
@@ -267,6 +270,148 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Addressing of the LDS DMA that moves one k-tile (64 k values) of the
+// implicit-GEMM operands: A rows (output pixels, gathered through the loader
+// LD) and B rows (packed weights [N][Kp]).  One DMA instruction moves 8 rows of
+// 8 16-byte chunks; this thread's instructions are A row-groups ga0 .. ga0+NA-1
+// and B row-groups gb0 .. gb0+NB-1.  Rows beyond M / N and padding taps read
+// the zero chunk in global memory instead, so the address arithmetic stays
+// branch-free.
+//
+// Lane l of row-group g fills row 8 g + l / 8, physical chunk l % 8, i.e.
+// logical chunk (l % 8) ^ ((row >> 1) & 7) = (l % 8) ^ ((4 g + l / 16) & 7).
+template <int NA, int NB, int LD>
+struct DmaPlan {
+  int roff[NA], rhi[NA], rwi[NA], rkc[NA], roff2[LD == LD_CAT ? NA : 1];
+  int boffs[NB];
+  bool bok[NB];
+  int ga0, gb0;
+
+  __device__ __forceinline__ void init(const ConvArgs &a, int m0, int n0, int ga, int gb, int lane) {
+    ga0 = ga;
+    gb0 = gb;
+    const int kcA = ((lane & 7) ^ ((lane >> 4) & 7)) * 8;        // even g
+    const int kcB = ((lane & 7) ^ ((4 + (lane >> 4)) & 7)) * 8;  // odd g
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      // Per-row gather state: element offset of the row's first tap (may
+      // point into padding) and the tap origin for bounds checks.
+      const int m = m0 + (ga + i) * 8 + (lane >> 3);
+      const RowState r = make_row<LD == LD_CAT ? LD_NHWC : LD>(a, m);
+      const int kc8 = ((ga + i) & 1) ? kcB : kcA;
+      rkc[i] = kc8;
+      rhi[i] = r.hi0;
+      rwi[i] = r.wi0;
+      if (LD == LD_NHWC || LD == LD_S2D || LD == LD_CAT)
+        roff[i] = r.base + (r.hi0 * a.W + r.wi0) * a.C + kc8;
+      else if (LD == LD_GEMM) roff[i] = r.base + kc8;
+      else roff[i] = r.base;
+      if (LD == LD_CAT) {
+        // shortcut pixel (n, ho * s2, wo * s2) of x2, relative to roff
+        const int hw = a.Ho * a.Wo;
+        const int mm = m < a.M ? m : 0;
+        const int n = mm / hw, rem = mm - n * hw;
+        const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
+        roff2[i] = ((n * a.H2 + ho * a.s2) * a.W2 + wo * a.s2) * a.C2 + kc8 - a.K1 - roff[i];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int n = n0 + (gb + j) * 8 + (lane >> 3);
+      bok[j] = n < a.N;
+      boffs[j] = (bok[j] ? n : 0) * a.Kp + (((gb + j) & 1) ? kcB : kcA);
+    }
+  }
+
+  // Moves instructions q0 <= q < q1 (A first, then B) of k-tile kt into the
+  // stage whose A and B parts start at As and Bs.
+  __device__ __forceinline__ void issue(const ConvArgs &a, int kt, uint16_t *As, uint16_t *Bs, int q0,
+                                        int q1) const {
+    const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero_chunk);
+    const uint16_t *x = static_cast<const uint16_t *>(a.x);
+    const uint16_t *wp = static_cast<const uint16_t *>(a.w);
+    const int kbase = kt * BK;
+    int kh_ = 0, kw_ = 0, tapoff = 0;
+    if (LD == LD_NHWC || LD == LD_CAT) {  // C % 64 == 0: the k-tile lies in one tap
+      const int tap = kbase / a.C;
+      kh_ = tap / a.kw;
+      kw_ = tap - kh_ * a.kw;
+      tapoff = (kh_ * a.W + kw_) * a.C + (kbase - tap * a.C);
+    }
+    // LD_CAT: k-tiles past K1 read the shortcut pixel of x2.  The first part
+    // is a stride-1 convolution at output resolution, so taps (pad, pad) are
+    // in bounds exactly for the real rows.  Both parts share one formula with
+    // uniform selectors, so the per-row arrays stay in registers.
+    const bool second = LD == LD_CAT && kbase >= a.K1;
+    const uint16_t *xs = second ? static_cast<const uint16_t *>(a.x2) : x;
+    const int cat_sel = second ? 1 : 0;
+    if (second) {
+      kh_ = kw_ = a.pad;
+      tapoff = kbase;
+    }
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      if (i < q0 || i >= q1) continue;
+      bool ok;
+      int off;
+      if (LD == LD_GEMM) {  // K % 8 == 0; chunks past K (ragged last k-tile) read zeros
+        ok = rhi[i] >= 0 && kbase + rkc[i] < a.K;
+        off = roff[i] + kbase;
+      } else if (LD == LD_NHWC || LD == LD_CAT) {
+        ok = (unsigned)(rhi[i] + kh_) < (unsigned)a.H && (unsigned)(rwi[i] + kw_) < (unsigned)a.W;
+        off = roff[i] + tapoff + (LD == LD_CAT ? cat_sel * roff2[i] : 0);
+      } else if (LD == LD_S2D) {
+        // k-tile kt is the contiguous run of cell row du = kt (kw x 16 = 64 elements)
+        ok = rhi[i] >= 0;
+        off = roff[i] + kt * a.W * a.C;
+      } else {  // LD_NCHW_PATCH: k = (c, u, v), 8 | kw
+        const int k0 = kbase + rkc[i];
+        const int khw = a.kh * a.kw;
+        const int c = k0 / khw, rem = k0 - c * khw;
+        const int u = rem / a.kw, vv = rem - u * a.kw;
+        ok = rhi[i] > -(1 << 27) && k0 < a.K;
+        off = roff[i] + (c * a.H + rhi[i] + u) * a.W + rwi[i] + vv;
+      }
+      const uint16_t *src = ok ? xs + off : zero;
+      __builtin_amdgcn_global_load_lds(src, LDS_PTR(As + (ga0 + i) * 512), 16, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      if (NA + j < q0 || NA + j >= q1) continue;
+      const uint16_t *src = bok[j] ? wp + boffs[j] + kbase : zero;
+      __builtin_amdgcn_global_load_lds(src, LDS_PTR(Bs + (gb0 + j) * 512), 16, 0, 0);
+    }
+  }
+};
+
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// Calls f(integral_constant<int, i>) for i = 0 .. N-1 (compile-time indices).
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Scheduling recipe of one MFMA k-step: NMF MFMAs with NRD fragment reads
+// and NDMA DMA issues (each with its address arithmetic) spread evenly
+// between them.
+template <int Q, int NMF, int NRD, int NDMA>
+__device__ __forceinline__ void sched_step() {
+  if constexpr (Q < NMF) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    constexpr int r0 = Q * NRD / NMF, r1 = (Q + 1) * NRD / NMF;
+    if constexpr (r1 > r0) __builtin_amdgcn_sched_group_barrier(0x100, r1 - r0, 0);  // DS read
+    constexpr int d0 = Q * NDMA / NMF, d1 = (Q + 1) * NDMA / NMF;
+    if constexpr (d1 > d0) {
+      __builtin_amdgcn_sched_group_barrier(0x002, 6 * (d1 - d0), 0);  // VALU
+      __builtin_amdgcn_sched_group_barrier(0x020, d1 - d0, 0);        // VMEM (DMA)
+    }
+    sched_step<Q + 1, NMF, NRD, NDMA>();
+  }
+}
+
 template <int BM, int BN, int STAGES, int EPI>
 struct PipeSmem {
   static constexpr int kStage = (BM + BN) * BK;  // elements per stage
@@ -298,102 +443,14 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  // Lane l of DMA instruction q (q = wave * NA + i, 8 rows of 8 chunks) fills
-  // row 8 q + l / 8, physical chunk l % 8, i.e. logical chunk
-  // (l % 8) ^ ((row >> 1) & 7) = (l % 8) ^ ((4 q + l / 16) & 7).
-  const int kcA = ((lane & 7) ^ ((lane >> 4) & 7)) * 8;        // even q
-  const int kcB = ((lane & 7) ^ ((4 + (lane >> 4)) & 7)) * 8;  // odd q
-  const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero_chunk);
-  const uint16_t *x = static_cast<const uint16_t *>(a.x);
-  const uint16_t *wp = static_cast<const uint16_t *>(a.w);
-
-  // Per-row gather state, computed once: element offset of the row's first
-  // tap (may point into padding), and the tap origin for bounds checks.
-  int roff[NA], rhi[NA], rwi[NA], rkc[NA], roff2[LD == LD_CAT ? NA : 1];
-  const uint16_t *x2 = static_cast<const uint16_t *>(a.x2);
-#pragma unroll
-  for (int i = 0; i < NA; ++i) {
-    const int m = m0 + (wave * NA + i) * 8 + (lane >> 3);
-    const RowState r = make_row<LD == LD_CAT ? LD_NHWC : LD>(a, m);
-    const int kc8 = ((wave * NA + i) & 1) ? kcB : kcA;
-    rkc[i] = kc8;
-    rhi[i] = r.hi0;
-    rwi[i] = r.wi0;
-    if (LD == LD_NHWC || LD == LD_S2D || LD == LD_CAT)
-      roff[i] = r.base + (r.hi0 * a.W + r.wi0) * a.C + kc8;
-    else if (LD == LD_GEMM) roff[i] = r.base + kc8;
-    else roff[i] = r.base;
-    if (LD == LD_CAT) {
-      // shortcut pixel (n, ho * s2, wo * s2) of x2
-      const int hw = a.Ho * a.Wo;
-      const int mm = m < a.M ? m : 0;
-      const int n = mm / hw, rem = mm - n * hw;
-      const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
-      roff2[i] = ((n * a.H2 + ho * a.s2) * a.W2 + wo * a.s2) * a.C2 + kc8 - a.K1;
-    }
-  }
-  int boffs[NB];
-  bool bok[NB];
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int n = n0 + (wave * NB + j) * 8 + (lane >> 3);
-    bok[j] = n < a.N;
-    boffs[j] = (bok[j] ? n : 0) * a.Kp + (((wave * NB + j) & 1) ? kcB : kcA);
-  }
+  DmaPlan<NA, NB, LD> dp;
+  dp.init(a, m0, n0, wave * NA, wave * NB, lane);
   const int nk = a.Kp / BK;
-
-  // Moves k-tile kt (< nk) into stage st.  Only per-lane conditions select
-  // the zero chunk, so the address arithmetic stays branch-free.
-  auto issue = [&](int kt, int st) {
+  // Only instructions q0 <= q < q1 of the tile's NA + NB (A first, then B)
+  // are issued, so the DMA of one k-tile can be spread over several k-steps.
+  auto issue = [&](int kt, int st, int q0, int q1) {
     uint16_t *As = smem + st * SM::kStage;
-    uint16_t *Bs = As + BM * BK;
-    const int kbase = kt * BK;
-    int kh_ = 0, kw_ = 0, tapoff = 0;
-    if (LD == LD_NHWC || LD == LD_CAT) {
-      const int tap = kbase / a.C;
-      kh_ = tap / a.kw;
-      kw_ = tap - kh_ * a.kw;
-      tapoff = (kh_ * a.W + kw_) * a.C + (kbase - tap * a.C);
-    }
-    const uint16_t *xs = (LD == LD_CAT && kbase >= a.K1) ? x2 : x;
-#pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      bool ok;
-      int off;
-      if (LD == LD_GEMM) {  // K % 8 == 0; chunks past K (ragged last k-tile) read zeros
-        ok = rhi[i] >= 0 && kbase + rkc[i] < a.K;
-        off = roff[i] + kbase;
-      } else if (LD == LD_NHWC) {
-        ok = (unsigned)(rhi[i] + kh_) < (unsigned)a.H && (unsigned)(rwi[i] + kw_) < (unsigned)a.W;
-        off = roff[i] + tapoff;
-      } else if (LD == LD_S2D) {
-        // k-tile kt is the contiguous run of cell row du = kt (kw x 16 = 64 elements)
-        ok = rhi[i] >= 0;
-        off = roff[i] + kt * a.W * a.C;
-      } else if (LD == LD_CAT) {
-        if (kbase < a.K1) {
-          ok = (unsigned)(rhi[i] + kh_) < (unsigned)a.H && (unsigned)(rwi[i] + kw_) < (unsigned)a.W;
-          off = roff[i] + tapoff;
-        } else {
-          ok = rhi[i] > -(1 << 27);
-          off = roff2[i] + kbase;
-        }
-      } else {  // LD_NCHW_PATCH: k = (c, u, v), 8 | kw
-        const int k0 = kbase + rkc[i];
-        const int khw = a.kh * a.kw;
-        const int c = k0 / khw, rem = k0 - c * khw;
-        const int u = rem / a.kw, vv = rem - u * a.kw;
-        ok = rhi[i] > -(1 << 27) && k0 < a.K;
-        off = roff[i] + (c * a.H + rhi[i] + u) * a.W + rwi[i] + vv;
-      }
-      const uint16_t *src = ok ? xs + off : zero;
-      __builtin_amdgcn_global_load_lds(src, LDS_PTR(As + (wave * NA + i) * 512), 16, 0, 0);
-    }
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const uint16_t *src = bok[j] ? wp + boffs[j] + kbase : zero;
-      __builtin_amdgcn_global_load_lds(src, LDS_PTR(Bs + (wave * NB + j) * 512), 16, 0, 0);
-    }
+    dp.issue(a, kt, As, As + BM * BK, q0, q1);
   };
 
   const int wm = wave / WN, wn = wave % WN;
@@ -418,39 +475,49 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
 
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
-    if (st < nk) issue(st, st);
+    if (st < nk) issue(st, st, 0, NA + NB);
 
   bf16x8_t af[2][TM], bfr[2][TN];
-  // One k-tile from LDS stage S: 4 MFMA k-steps, the next step's fragments
-  // read while the current step's MFMAs run.  `pre` issues the DMA of a later
-  // k-tile after the first fragments are read.
-  auto run_tile = [&](const uint16_t *S, auto &&pre) {
+  auto read_frags = [&](const uint16_t *S, int ks, int buf) {
+    const int ch = ((2 * ks + lh) ^ sw) * 8;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-      af[0][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ((lh ^ sw) * 8));
+    for (int i = 0; i < TM; ++i) af[buf][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
-      bfr[0][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ((lh ^ sw) * 8));
-    pre();
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int cur = ks & 1;
-      if (ks + 1 < KS) {
-        const int ch = ((2 * (ks + 1) + lh) ^ sw) * 8;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          af[cur ^ 1][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[cur ^ 1][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
-      }
+    for (int j = 0; j < TN; ++j) bfr[buf][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
+  };
+  // One k-tile from LDS stage S: KS MFMA k-steps; step ks reads the
+  // fragments of step ks + 1 while its MFMAs run.  With a DMA (WITH_DMA), the
+  // instructions of a later k-tile are spread evenly over the first KS - 1
+  // steps: the memory pipeline accepts about one 1 KB DMA per 16 clocks per CU,
+  // and a burst would stall the issuing wave (and its MFMAs) on a full queue;
+  // the last step is left as slack for the DMAs to land.
+  // With SCHED each step is its own scheduling region in which the reads and
+  // DMA issues are placed between the MFMAs, so one wait per step covers the
+  // next step's operands.
+  auto run_tile = [&](const uint16_t *S, int kn, int sn, auto with_dma) {
+    constexpr bool WITH_DMA = decltype(with_dma)::value;
+    read_frags(S, 0, 0);
+    if (SCHED) __builtin_amdgcn_sched_barrier(0);
+    static_for<KS>([&](auto ksc) {
+      constexpr int ks = decltype(ksc)::value;
+      constexpr int cur = ks & 1;
+      if constexpr (ks + 1 < KS) read_frags(S, ks + 1, cur ^ 1);
+      constexpr int NDS = KS > 1 ? KS - 1 : 1, NQ = NA + NB;
+      constexpr int q0 = !WITH_DMA || ks >= NDS ? 0 : ks * NQ / NDS;
+      constexpr int q1 = !WITH_DMA || ks >= NDS ? 0 : (ks + 1) * NQ / NDS;
+      if constexpr (q1 > q0) issue(kn, sn, q0, q1);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = EPI ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0)
                           : __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
-    }
+      if constexpr (SCHED != 0) {
+        constexpr int ndma = q1 - q0;
+        sched_step<0, TM * TN, (ks + 1 < KS) ? TM + TN : 0, ndma>();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    });
   };
 
   int kt = 0;
@@ -459,31 +526,15 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   for (; kt + STAGES - 1 < nk; ++kt) {
     wait_vmcnt<(STAGES - 2) * (NA + NB)>();
     __builtin_amdgcn_s_barrier();
-    run_tile(smem + (kt % STAGES) * SM::kStage,
-             [&] { issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES); });
-    if (SCHED) {
-      // Spread the next k-steps' LDS reads and the DMA issue (address
-      // arithmetic + global_load_lds) between the MFMAs of this k-tile.
-      constexpr int NMF = KS * TM * TN;
-      constexpr int NRD = (KS - 1) * (TM + TN);
-      constexpr int NDMA = NA + NB;
-#pragma unroll
-      for (int q = 0; q < NMF; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
-        if (q < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // DS read
-        if (q < NDMA) {
-          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);               // VALU
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);               // VMEM (DMA)
-        }
-      }
-    }
+    const int kn = kt + STAGES - 1;
+    run_tile(smem + (kt % STAGES) * SM::kStage, kn, kn % STAGES, std::true_type{});
   }
   // Drain: no more tiles to issue.
   for (; kt < nk; ++kt) {
     if (STAGES >= 3 && nk - 1 - kt >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * (NA + NB)>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    run_tile(smem + (kt % STAGES) * SM::kStage, [] {});
+    run_tile(smem + (kt % STAGES) * SM::kStage, 0, 0, std::false_type{});
   }
   if (EPI) {
     // acc[i][j][4g + e] = C[m][n + e], m = block row + lane % 32,
@@ -573,6 +624,326 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   }
 }
 
+// ------------------------------------------ bf16, warp-specialised pipeline
+//
+// WM x WN consumer waves only read fragments and run MFMAs; as many producer
+// waves move the k-tiles STAGES - 1 ahead into LDS with buffer loads that
+// write LDS directly.  A SIMD whose MFMA pipe is kept busy by one wave issues
+// VALU instructions of its other waves only rarely, so the producers' steady
+// state holds no VALU instruction at all: every per-lane byte offset is
+// computed once (one per kernel tap), padding taps and rows beyond M / N get
+// an offset outside the buffer's range, for which the hardware writes zeros,
+// and a k-tile only moves scalar values (the LDS address in M0 and the
+// buffer's scalar offset).  One s_barrier per k-tile, reached by all waves,
+// hands a landed stage to the consumers and a consumed stage back to the
+// producers.
+constexpr unsigned kOob = 0x80000000u;  // a byte offset outside every buffer range
+
+// Moves 16 bytes per lane from base + soff + voff (a raw buffer of 2^31 - 1
+// bytes: offsets at or beyond kOob read zeros) into LDS at lds + 16 * lane.
+// Only scalar instructions besides the load itself.
+__device__ __forceinline__ void dma16(const void *base, uint16_t *lds, unsigned voff, unsigned soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7fffffff, 0x00020000), LDS_PTR(lds), 16,
+      voff, soff, 0, 0);
+}
+
+// Per-lane offsets of one producer lane.  Row-group g = ga + i (A) or gb + j
+// (B) covers rows 8 g .. 8 g + 7; lane l moves row 8 g + l / 8 and logical
+// chunk (l % 8) ^ ((row >> 1) & 7) of the 64-wide k-tile, as in DmaPlan.
+template <int NA, int NB, int LD, int KW>
+struct WsPlan {
+  static constexpr int TAPS = (LD == LD_NHWC || LD == LD_CAT) ? KW * KW : 1;
+  unsigned va[TAPS][NA];                // A, first part: per kernel tap
+  unsigned va2[LD == LD_CAT ? NA : 1];  // LD_CAT: shortcut pixel (n, ho s2, wo s2) of x2
+  unsigned vb[NB];
+
+  __device__ __forceinline__ void init(const ConvArgs &a, int m0, int n0, int ga, int gb, int lane) {
+    const int kcA = ((lane & 7) ^ ((lane >> 4) & 7)) * 8;        // even g
+    const int kcB = ((lane & 7) ^ ((4 + (lane >> 4)) & 7)) * 8;  // odd g
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int m = m0 + (ga + i) * 8 + (lane >> 3);
+      const int kc8 = ((ga + i) & 1) ? kcB : kcA;
+      const bool valid = m < a.M;
+      const int hw = a.Ho * a.Wo;
+      const int mm = valid ? m : 0;
+      const int n = mm / hw, rem = mm - n * hw;
+      const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
+      if (LD == LD_GEMM) {
+        va[0][i] = valid ? (unsigned)(((int64_t)m * a.K + kc8) * 2) : kOob;
+      } else if (LD == LD_S2D) {  // k-tile du adds du * W * C (scalar)
+        va[0][i] = valid ? (unsigned)(((((int64_t)n * a.H + ho) * a.W + wo) * a.C + kc8) * 2) : kOob;
+      } else if (LD == LD_NCHW_PATCH) {  // kw == 16: k-tile = 4 kernel rows of one channel
+        const int du = kc8 >> 4, dv = kc8 & 15;
+        va[0][i] = valid ? (unsigned)((((int64_t)n * a.C * a.H + ho * a.kh + du) * a.W + wo * a.kw + dv) * 2)
+                         : kOob;
+      } else {  // LD_NHWC, LD_CAT first part
+#pragma unroll
+        for (int tap = 0; tap < TAPS; ++tap) {
+          const int hi = ho * a.stride - a.pad + tap / KW, wi = wo * a.stride - a.pad + tap % KW;
+          const bool in = valid && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
+          va[tap][i] = in ? (unsigned)(((((int64_t)n * a.H + hi) * a.W + wi) * a.C + kc8) * 2) : kOob;
+        }
+        if (LD == LD_CAT)
+          va2[LD == LD_CAT ? i : 0] =
+              valid ? (unsigned)(((((int64_t)n * a.H2 + ho * a.s2) * a.W2 + wo * a.s2) * a.C2 + kc8) * 2) : kOob;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int n = n0 + (gb + j) * 8 + (lane >> 3);
+      vb[j] = n < a.N ? (unsigned)(((int64_t)n * a.Kp + (((gb + j) & 1) ? kcB : kcA)) * 2) : kOob;
+    }
+  }
+};
+
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI>
+__device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
+  constexpr int CW = WM * WN;                      // consumer waves (= producer waves)
+  constexpr int NT = 2 * CW * 64;
+  constexpr int TM = BM / (WM * 32), TN = BN / (WN * 32);
+  constexpr int NA = BM / (8 * CW), NB = BN / (8 * CW);  // DMA instructions per producer lane
+  constexpr int NQ = NA + NB;
+  constexpr int KS = BK / 16;
+  using SM = PipeSmem<BM, BN, STAGES, EPI>;
+  using Plan = WsPlan<NA, NB, LD, KW>;
+  static_assert(NA * 8 * CW == BM && NB * 8 * CW == BN && TM >= 1 && TN >= 1, "tile");
+  static_assert(STAGES >= 2 && STAGES <= 4 && (STAGES - 2) * NQ < 64, "stages");
+  __shared__ __attribute__((aligned(16))) uint8_t smem_raw[SM::kBytes];
+  uint16_t *smem = reinterpret_cast<uint16_t *>(smem_raw);
+
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // uniform: keeps LDS addresses scalar
+  const bool producer = wave >= CW;
+  const int nk = a.Kp / BK;
+
+  const int wm = (wave % CW) / WN, wn = (wave % CW) % WN;
+  const int lrow = lane & 31, lh = lane >> 5;
+  f32x16_t acc[TM][TN];
+
+  if (producer) {
+    const int pw = wave - CW;
+    Plan pl;
+    pl.init(a, m0, n0, pw * NA, pw * NB, lane);
+    // k-tiles per tap of the first part; the scalar A offset of k-tile (tap, cb)
+    const int cpt = (LD == LD_NHWC || LD == LD_CAT) ? a.C / BK : nk;
+    auto soff_a = [&](int cb) -> unsigned {
+      if (LD == LD_GEMM || LD == LD_NHWC || LD == LD_CAT) return (unsigned)(cb * BK * 2);
+      if (LD == LD_S2D) return (unsigned)(cb * a.W * a.C * 2);
+      // LD_NCHW_PATCH: channel c = cb / (kh / 4), kernel rows u0 = 4 (cb % (kh / 4))
+      const int rpc = a.kh / 4, c = cb / rpc, u0 = (cb - c * rpc) * 4;
+      return (unsigned)((((int64_t)c * a.H + u0) * a.W) * 2);
+    };
+    int q = 0;  // next k-tile to issue
+    // Before issuing k-tile q into stage q % STAGES: once STAGES - 1 tiles are
+    // in flight, wait until k-tile q - STAGES + 1 has landed, then meet the
+    // consumers at its barrier (which also frees the stage it reuses).
+    auto gate = [&] {
+      if (q >= STAGES - 1) {
+        wait_vmcnt<(STAGES - 2) * NQ>();
+        __builtin_amdgcn_s_barrier();
+      }
+    };
+    auto issue_b = [&](uint16_t *Bs) {
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        dma16(a.w, Bs + (pw * NB + j) * 512, pl.vb[j], (unsigned)(q * BK * 2));
+    };
+    static_for<Plan::TAPS>([&](auto tc) {
+      constexpr int tap = decltype(tc)::value;
+      for (int cb = 0; cb < cpt; ++cb) {
+        gate();
+        uint16_t *As = smem + (q % STAGES) * SM::kStage;
+        const unsigned so = soff_a(cb);
+#pragma unroll
+        for (int i = 0; i < NA; ++i)
+          dma16(a.x, As + (pw * NA + i) * 512, pl.va[tap][i], so);
+        issue_b(As + BM * BK);
+        ++q;
+      }
+    });
+    if (LD == LD_CAT) {  // shortcut part: 1 x 1 on x2
+      const int cpt2 = a.C2 / BK;
+      for (int cb = 0; cb < cpt2; ++cb) {
+        gate();
+        uint16_t *As = smem + (q % STAGES) * SM::kStage;
+#pragma unroll
+        for (int i = 0; i < NA; ++i)
+          dma16(a.x2, As + (pw * NA + i) * 512, pl.va2[LD == LD_CAT ? i : 0], (unsigned)(cb * BK * 2));
+        issue_b(As + BM * BK);
+        ++q;
+      }
+    }
+    // Drain: the last min(nk, STAGES - 1) barriers; k-tile b has nk - 1 - b
+    // younger tiles in flight.
+    for (int b = max(0, nk - STAGES + 1); b < nk; ++b) {
+      const int younger = nk - 1 - b;
+      if (STAGES >= 4 && younger >= 2) wait_vmcnt<(STAGES >= 4 ? 2 : 0) * NQ>();
+      else if (STAGES >= 3 && younger >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * NQ>();
+      else wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    // Fragment offsets inside a stage; k-step ks reads logical chunk 2 ks + lh,
+    // stored at physical chunk (2 ks + lh) ^ ((row >> 1) & 7).
+    int aoff[TM], boff[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) aoff[i] = (wm * TM * 32 + i * 32 + lrow) * BK;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) boff[j] = BM * BK + (wn * TN * 32 + j * 32 + lrow) * BK;
+    const int sw = (lrow >> 1) & 7;
+    bf16x8_t af[2][TM], bfr[2][TN];
+    auto read_frags = [&](const uint16_t *S, int ks, int buf) {
+      const int ch = ((2 * ks + lh) ^ sw) * 8;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[buf][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bfr[buf][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
+    };
+    for (int kt = 0; kt < nk; ++kt) {
+      __builtin_amdgcn_s_barrier();
+      const uint16_t *S = smem + (kt % STAGES) * SM::kStage;
+      read_frags(S, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      static_for<KS>([&](auto ksc) {
+        constexpr int ks = decltype(ksc)::value;
+        constexpr int cur = ks & 1;
+        if constexpr (ks + 1 < KS) read_frags(S, ks + 1, cur ^ 1);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = EPI ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0)
+                            : __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+        sched_step<0, TM * TN, (ks + 1 < KS) ? TM + TN : 0, 0>();
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
+  }
+
+  uint16_t *y = static_cast<uint16_t *>(a.y);
+  const uint16_t *res = static_cast<const uint16_t *>(a.res);
+  if (EPI) {
+    if (producer) return;
+    // acc[i][j][4g + e] = C[m][n + e], m = block row + lane % 32,
+    // n = block column + 8 g + 4 (lane / 32).
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = n0 + wn * TN * 32 + j * 32 + 8 * g + 4 * lh;
+        if (n >= a.N) continue;
+        const float4 bv = a.bias ? *reinterpret_cast<const float4 *>(a.bias + n)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int m = m0 + wm * TM * 32 + i * 32 + lrow;
+          if (m >= a.M) continue;
+          float v[4] = {acc[i][j][4 * g] + bv.x, acc[i][j][4 * g + 1] + bv.y,
+                        acc[i][j][4 * g + 2] + bv.z, acc[i][j][4 * g + 3] + bv.w};
+          if (res) {
+            const uint2 rv = *reinterpret_cast<const uint2 *>(res + (int64_t)m * a.ldr + n);
+            v[0] += bf2f((uint16_t)(rv.x & 0xffff));
+            v[1] += bf2f((uint16_t)(rv.x >> 16));
+            v[2] += bf2f((uint16_t)(rv.y & 0xffff));
+            v[3] += bf2f((uint16_t)(rv.y >> 16));
+          }
+          uint2 o;
+          o.x = f2bf(epilogue_act(v[0], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[1], a.relu, a.gelu)) << 16);
+          o.y = f2bf(epilogue_act(v[2], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[3], a.relu, a.gelu)) << 16);
+          *reinterpret_cast<uint2 *>(y + (int64_t)m * a.ldc + n) = o;
+        }
+      }
+    }
+    return;
+  }
+
+  // Epilogue: the consumers stage the fp32 tile in LDS (the stages are free:
+  // every DMA has landed and every fragment was read before this barrier),
+  // then all waves finish 8 consecutive output channels of a row per thread
+  // and store them as one 16-byte write.
+  __syncthreads();
+  float *Cs = reinterpret_cast<float *>(smem_raw);
+  if (!producer) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * TM * 32 + i * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+          const int col = wn * TN * 32 + j * 32 + lrow;
+          Cs[row * SM::kCPitch + col] = acc[i][j][r];
+        }
+  }
+  __syncthreads();
+  constexpr int CPR = BN / 8;    // 8-column chunks per row
+  constexpr int RPP = NT / CPR;  // rows per pass
+  const int cc = t % CPR;
+  const int n = n0 + cc * 8;
+  if (n >= a.N) return;
+  float bias[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bias[e] = a.bias ? a.bias[n + e] : 0.0f;
+#pragma unroll 4
+  for (int rr = t / CPR; rr < BM; rr += RPP) {
+    const int m = m0 + rr;
+    if (m >= a.M) break;
+    const float4 p = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8);
+    const float4 q = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8 + 4);
+    float v[8] = {p.x, p.y, p.z, p.w, q.x, q.y, q.z, q.w};
+    if (res) {
+      const uint4 rv = *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n);
+      const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] += bf2f((uint16_t)(w4[e] & 0xffff));
+        v[2 * e + 1] += bf2f((uint16_t)(w4[e] >> 16));
+      }
+    }
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = epilogue_act(v[2 * e] + bias[2 * e], a.relu, a.gelu);
+      const float hi = epilogue_act(v[2 * e + 1] + bias[2 * e + 1], a.relu, a.gelu);
+      o[e] = f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+    }
+    *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// One workgroup per CU (large tiles), or two (the register budget halves).
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI>
+__global__ __launch_bounds__(2 * WM * WN * 64) void conv_bf16_ws_kernel(ConvArgs a) {
+  conv_bf16_ws_body<BM, BN, WM, WN, STAGES, LD, KW, EPI>(a);
+}
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI>
+__global__ __launch_bounds__(2 * WM * WN * 64, 2) void conv_bf16_ws2_kernel(ConvArgs a) {
+  conv_bf16_ws_body<BM, BN, WM, WN, STAGES, LD, KW, EPI>(a);
+}
+
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 0, int MINB = 1>
+hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  if constexpr (MINB >= 2)
+    hipLaunchKernelGGL((conv_bf16_ws2_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
+                       dim3(2 * WM * WN * 64), 0, s, a);
+  else
+    hipLaunchKernelGGL((conv_bf16_ws_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
+                       dim3(2 * WM * WN * 64), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int LD>
 hipError_t launch_bf16_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
@@ -588,6 +959,35 @@ hipError_t launch_pipe_cfg(const ConvArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Whether the warp-specialised kernel handles this launch: whole 64-wide
+// k-tiles, kernel taps it was built for, and every operand addressable with
+// 31-bit byte offsets.
+bool ws_eligible(const ConvArgs &a, Loader ld) {
+  const int64_t lim = (int64_t)1 << 31;
+  if ((int64_t)a.N * a.Kp * 2 >= lim) return false;
+  switch (ld) {
+    case LD_GEMM: return a.K % BK == 0 && (int64_t)a.M * a.K * 2 < lim;
+    case LD_NHWC:
+    case LD_CAT:
+      if (a.C % BK != 0 || a.kh != a.kw || (a.kh != 1 && a.kh != 3)) return false;
+      if ((int64_t)a.n_img * a.H * a.W * a.C * 2 >= lim) return false;
+      return ld == LD_NHWC || (a.C2 % BK == 0 && (int64_t)a.n_img * a.H2 * a.W2 * a.C2 * 2 < lim);
+    case LD_S2D: return (int64_t)a.n_img * a.H * a.W * a.C * 2 < lim;
+    case LD_NCHW_PATCH:
+      return a.kw == 16 && a.kh % 4 == 0 && (int64_t)a.n_img * a.C * a.H * a.W * 2 < lim;
+    default: return false;
+  }
+}
+
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int EPI, int MINB>
+hipError_t launch_ws_ld(const ConvArgs &a, hipStream_t s) {
+  if (LD == LD_NHWC || LD == LD_CAT) {
+    if (a.kh == 3) return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, 3, EPI, MINB>(a, s);
+    return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, 1, EPI, MINB>(a, s);
+  }
+  return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, 1, EPI, MINB>(a, s);
+}
+
 // Tuning override: HAPI_CONV_CFG=<index> forces one tile configuration.
 int forced_cfg() {
   static const int v = [] {
@@ -601,7 +1001,9 @@ int forced_cfg() {
 // choice never changes a result bit.
 template <int LD>
 hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
-  switch (forced_cfg()) {
+  const int fc = forced_cfg();
+  if (fc >= 20 && !ws_eligible(a, (Loader)LD)) return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);
+  switch (fc) {
     case 0: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);
     case 1: return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1, 0>(a, s);
     case 2: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 1>(a, s);
@@ -614,12 +1016,26 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     case 9: return launch_pipe_cfg<128, 128, 2, 2, 3, LD, 1, 1>(a, s);
     case 10: return launch_pipe_cfg<256, 64, 4, 1, 2, LD, 1, 1>(a, s);
     case 11: return launch_pipe_cfg<64, 128, 1, 4, 3, LD, 1, 1>(a, s);
+    case 12: return launch_pipe_cfg<256, 256, 2, 2, 2, LD, 1, 1>(a, s);
+    case 20: return launch_ws_ld<256, 128, 2, 2, 3, LD, 0, 1>(a, s);
+    case 21: return launch_ws_ld<128, 128, 2, 2, 4, LD, 0, 1>(a, s);
+    case 22: return launch_ws_ld<128, 256, 2, 2, 3, LD, 0, 1>(a, s);
+    case 23: return launch_ws_ld<256, 64, 4, 1, 4, LD, 0, 1>(a, s);
+    case 24: return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+    case 25: return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
     default: break;
   }
-  // Measured on MI355X over the ResNet-50 conv shapes: two or three
-  // workgroups per CU beat larger single-workgroup tiles for every shape; the
-  // direct-store epilogue (48 KB of LDS, 3 workgroups per CU) wins only for
-  // 64-channel outputs with long K.
+  // Measured on MI355X over the ResNet-50 conv shapes.  With at least two
+  // k-tiles the warp-specialised kernel (two workgroups per CU) wins; for a
+  // single k-tile its extra synchronisation does not pay.  For 64-channel
+  // outputs with short K the three-stage pipelined kernel stays ahead.
+  if (a.K >= 2 * BK && ws_eligible(a, (Loader)LD)) {
+    if (a.N <= 64) {
+      if (a.K >= 512) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+    } else {
+      return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+    }
+  }
   if (a.N <= 64) {
     if (a.K > 256) return launch_pipe_cfg<128, 64, 2, 2, 2, LD, 1, 1>(a, s);
     return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1, 0>(a, s);
