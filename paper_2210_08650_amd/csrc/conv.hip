@@ -473,6 +473,24 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  // The residual block this thread adds in the staged epilogue, loaded
+  // before the first DMA (so it is older than every DMA the k-loop waits
+  // for): its latency overlaps the whole k-loop instead of the epilogue.
+  constexpr int CPR = BN / 8;   // 8-column chunks per row
+  constexpr int RPP = NT / CPR; // rows per pass
+  constexpr int RPT = BM / RPP; // rows per thread
+  uint4 rpre[EPI ? 1 : RPT];
+  if (!EPI && a.res) {
+    const uint16_t *res = static_cast<const uint16_t *>(a.res);
+    const int n = n0 + (t % CPR) * 8;
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      const int m = m0 + t / CPR + k * RPP;
+      rpre[k] = (m < a.M && n < a.N) ? *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n)
+                                      : make_uint4(0, 0, 0, 0);
+    }
+  }
+
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < nk) issue(st, st, 0, NA + NB);
@@ -587,8 +605,6 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
         Cs[row * SM::kCPitch + col] = acc[i][j][r];
       }
   __syncthreads();
-  constexpr int CPR = BN / 8;             // 8-column chunks per row
-  constexpr int RPP = NT / CPR;           // rows per pass
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
   if (n >= a.N) return;
@@ -596,16 +612,16 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
 #pragma unroll
   for (int e = 0; e < 8; ++e) bias[e] = a.bias ? a.bias[n + e] : 0.0f;
   uint16_t *y = static_cast<uint16_t *>(a.y);
-  const uint16_t *res = static_cast<const uint16_t *>(a.res);
-#pragma unroll 4
-  for (int rr = t / CPR; rr < BM; rr += RPP) {
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int rr = t / CPR + k * RPP;
     const int m = m0 + rr;
     if (m >= a.M) break;
     const float4 p = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8);
     const float4 q = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8 + 4);
     float v[8] = {p.x, p.y, p.z, p.w, q.x, q.y, q.z, q.w};
-    if (res) {
-      const uint4 rv = *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n);
+    if (a.res) {
+      const uint4 rv = rpre[EPI ? 0 : k];
       const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -738,6 +754,24 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   const int wm = (wave % CW) / WN, wn = (wave % CW) % WN;
   const int lrow = lane & 31, lh = lane >> 5;
   f32x16_t acc[TM][TN];
+
+  // Residual rows of the staged epilogue, loaded before any DMA (so they are
+  // older than every DMA a producer waits for): the latency overlaps the
+  // k-loop instead of the epilogue.
+  constexpr int CPR = BN / 8;    // 8-column chunks per row
+  constexpr int RPP = NT / CPR;  // rows per pass
+  constexpr int RPT = BM / RPP;  // rows per thread
+  uint4 rpre[EPI ? 1 : RPT];
+  if (!EPI && a.res) {
+    const uint16_t *res = static_cast<const uint16_t *>(a.res);
+    const int n = n0 + (t % CPR) * 8;
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      const int m = m0 + t / CPR + k * RPP;
+      rpre[k] = (m < a.M && n < a.N) ? *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n)
+                                      : make_uint4(0, 0, 0, 0);
+    }
+  }
 
   if (producer) {
     const int pw = wave - CW;
@@ -901,23 +935,22 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
         }
   }
   __syncthreads();
-  constexpr int CPR = BN / 8;    // 8-column chunks per row
-  constexpr int RPP = NT / CPR;  // rows per pass
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
   if (n >= a.N) return;
   float bias[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) bias[e] = a.bias ? a.bias[n + e] : 0.0f;
-#pragma unroll 4
-  for (int rr = t / CPR; rr < BM; rr += RPP) {
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int rr = t / CPR + k * RPP;
     const int m = m0 + rr;
     if (m >= a.M) break;
     const float4 p = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8);
     const float4 q = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8 + 4);
     float v[8] = {p.x, p.y, p.z, p.w, q.x, q.y, q.z, q.w};
     if (res) {
-      const uint4 rv = *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n);
+      const uint4 rv = rpre[EPI ? 0 : k];
       const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
