@@ -5,7 +5,7 @@ the library's HIP kernels.  Device pointers are passed as integers or as
 objects with a ``data_ptr()`` method (torch tensors); streams as integers or
 objects with a ``cuda_stream`` attribute.  A negative status raises
 ``HapiError`` carrying the library's message.  The library must be built
-(``python -m paper_2210_08650_amd.build``); importing without it fails.
+(``python paper_2210_08650_amd/build.py``); importing without it fails.
 """
 from __future__ import annotations
 
@@ -71,7 +71,7 @@ def _hip_runtimes():
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2210_08650_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2210_08650_amd/build.py`")
     # libhapi must share torch's HIP runtime (streams and device pointers come
     # from torch).  Importing torch first maps torch's libamdhip64, whose soname
     # then satisfies libhapi's dependency; loading libhapi first would map a

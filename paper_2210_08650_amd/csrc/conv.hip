@@ -1006,6 +1006,334 @@ hipError_t launch_pipe_cfg(const ConvArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ------------------------------- bf16, persistent warp-specialised pipeline
+//
+// As the warp-specialised kernel, but one workgroup per CU processes a
+// contiguous range of output tiles, and its PW producer waves stream the
+// k-tiles of consecutive tiles through one STAGES-deep ring.  The ring never
+// drains between tiles: the first k-tiles of the next tile load while the
+// WM x WN consumer waves finish the current one, so layers with a few k-tiles
+// per tile no longer pay the pipeline fill once per tile.  Consumers prefetch
+// the residual of a tile into registers before its first k-tile, so its
+// latency overlaps the whole k-loop.  The MFMA operands are swapped (weights
+// as A) so that a lane's accumulators hold 4 consecutive output channels of
+// one pixel.  Epilogue EP = 0 stores those 8 bytes per lane directly; EP = 1
+// finishes 32-row slabs in a private LDS area per wave and stores 16-byte
+// row chunks; EP = 2 exchanges accumulator halves between the two half-waves
+// (v_permlane32_swap) so that every lane owns 8 consecutive channels of one
+// pixel, then loads the residual and stores the result as 16-byte chunks,
+// without LDS.
+template <int BM, int BN, int WM, int WN, int PW, int STAGES, int LD, int KW, int EP>
+__global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(ConvArgs a) {
+  constexpr int CW = WM * WN;                             // consumer waves
+  constexpr int TM = BM / (WM * 32), TN = BN / (WN * 32);
+  constexpr int NA = BM / (8 * PW), NB = BN / (8 * PW);   // DMA instructions per producer lane
+  constexpr int NQ = NA + NB;
+  constexpr int KS = BK / 16;
+  constexpr int kStage = (BM + BN) * BK;                  // elements per stage
+  constexpr int kWC = TN * 32;                            // columns of a consumer wave's block
+  constexpr int kEP = kWC + 8;                            // bf16 pitch of a staged slab row
+  constexpr int kSlab = EP == 1 ? 32 * kEP : 0;           // elements of a wave's slab
+  using Plan = WsPlan<NA, NB, LD, KW>;
+  static_assert(NA * 8 * PW == BM && NB * 8 * PW == BN && TM >= 1 && TN >= 1, "tile");
+  static_assert(STAGES >= 2 && STAGES <= 6 && (STAGES - 2) * NQ < 64, "stages");
+  static_assert((STAGES * kStage + CW * kSlab) * 2 <= 163840, "LDS");
+  static_assert((CW + PW) * 64 <= 1024, "workgroup size");
+  // The bias is read from LDS in the epilogue: a global load there would sit
+  // behind the wave's earlier stores in the one vector-memory counter, and
+  // every wait for it would also wait for those stores to be acknowledged.
+  constexpr int kLdsUsed = (STAGES * kStage + CW * kSlab) * 2;
+  constexpr int kBiasMax = (163840 - kLdsUsed) / 4 < 4096 ? (163840 - kLdsUsed) / 4 : 4096;
+  static_assert(kBiasMax >= 256, "LDS for the bias");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[STAGES * kStage + CW * kSlab];
+  __shared__ __attribute__((aligned(16))) float bias_s[kBiasMax];
+
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int tiles = ((a.M + BM - 1) / BM) * tiles_n;
+  const int G = gridDim.x;
+  // Logical workgroup index: consecutive indices share an XCD (and its L2),
+  // so an XCD works through one contiguous range of tiles.
+  const int wg = xcd_remap(blockIdx.x, G);
+  const int t_lo = (int)((int64_t)tiles * wg / G), t_hi = (int)((int64_t)tiles * (wg + 1) / G);
+  const int nk = a.Kp / BK;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // uniform: keeps LDS addresses scalar
+  // Bias in LDS when it fits (one barrier, met by every wave before the
+  // producer / consumer split); zero when absent.
+  const bool bias_lds = a.N <= kBiasMax;
+  if (bias_lds) {
+    for (int c = t; c < a.N; c += (CW + PW) * 64) bias_s[c] = a.bias ? a.bias[c] : 0.0f;
+    __syncthreads();
+  }
+
+  if (wave >= CW) {
+    // ---- producers: k-tile q of the workgroup's stream goes to stage q % STAGES.
+    const int pw = wave - CW;
+    const int cpt = (LD == LD_NHWC || LD == LD_CAT) ? a.C / BK : nk;  // k-tiles per tap
+    auto soff_a = [&](int cb) -> unsigned {
+      if (LD == LD_GEMM || LD == LD_NHWC || LD == LD_CAT) return (unsigned)(cb * BK * 2);
+      if (LD == LD_S2D) return (unsigned)(cb * a.W * a.C * 2);
+      const int rpc = a.kh / 4, c = cb / rpc, u0 = (cb - c * rpc) * 4;  // LD_NCHW_PATCH
+      return (unsigned)((((int64_t)c * a.H + u0) * a.W) * 2);
+    };
+    int q = 0;
+    // Before issuing k-tile q: once STAGES - 1 are in flight, wait until k-tile
+    // q - STAGES + 1 has landed and meet the consumers at its barrier, which
+    // also frees the stage that k-tile q reuses.
+    auto gate = [&] {
+      if (q >= STAGES - 1) {
+        wait_vmcnt<(STAGES - 2) * NQ>();
+        __builtin_amdgcn_s_barrier();
+      }
+    };
+    for (int tile = t_lo; tile < t_hi; ++tile) {
+      const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+      Plan pl;
+      pl.init(a, m0, n0, pw * NA, pw * NB, lane);
+      int kq = 0;  // k-tile within the tile
+      auto issue_b = [&](uint16_t *Bs) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          dma16(a.w, Bs + (pw * NB + j) * 512, pl.vb[j], (unsigned)(kq * BK * 2));
+      };
+      static_for<Plan::TAPS>([&](auto tc) {
+        constexpr int tap = decltype(tc)::value;
+        for (int cb = 0; cb < cpt; ++cb) {
+          gate();
+          uint16_t *As = smem + (q % STAGES) * kStage;
+          const unsigned so = soff_a(cb);
+#pragma unroll
+          for (int i = 0; i < NA; ++i) dma16(a.x, As + (pw * NA + i) * 512, pl.va[tap][i], so);
+          issue_b(As + BM * BK);
+          ++q;
+          ++kq;
+        }
+      });
+      if (LD == LD_CAT) {  // shortcut part: 1 x 1 on x2
+        const int cpt2 = a.C2 / BK;
+        for (int cb = 0; cb < cpt2; ++cb) {
+          gate();
+          uint16_t *As = smem + (q % STAGES) * kStage;
+#pragma unroll
+          for (int i = 0; i < NA; ++i)
+            dma16(a.x2, As + (pw * NA + i) * 512, pl.va2[LD == LD_CAT ? i : 0], (unsigned)(cb * BK * 2));
+          issue_b(As + BM * BK);
+          ++q;
+          ++kq;
+        }
+      }
+    }
+    // Drain: the last min(q, STAGES - 1) barriers; k-tile b has q - 1 - b
+    // younger k-tiles in flight.
+    for (int b = max(0, q - STAGES + 1); b < q; ++b) {
+      const int younger = q - 1 - b;
+      static_for<STAGES - 1>([&](auto yc) {
+        constexpr int yv = decltype(yc)::value;
+        if (younger == yv) wait_vmcnt<yv * NQ>();
+      });
+      __builtin_amdgcn_s_barrier();
+    }
+    return;  // every barrier of the stream has been met
+  }
+
+  // ---- consumers
+  const int wm = wave / WN, wn = wave % WN;
+  const int lrow = lane & 31, lh = lane >> 5;
+  const int sw = (lrow >> 1) & 7;
+  // Fragment offsets inside a stage; k-step ks reads logical chunk 2 ks + lh,
+  // stored at physical chunk (2 ks + lh) ^ ((row >> 1) & 7).
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) aoff[i] = (wm * TM * 32 + i * 32 + lrow) * BK;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) boff[j] = BM * BK + (wn * kWC + j * 32 + lrow) * BK;
+  uint16_t *y = static_cast<uint16_t *>(a.y);
+  const uint16_t *res = static_cast<const uint16_t *>(a.res);
+  uint16_t *slab = smem + STAGES * kStage + wave * kSlab;
+  bf16x8_t af[2][TM], bfr[2][TN];
+  auto read_frags = [&](const uint16_t *S, int ks, int buf) {
+    const int ch = ((2 * ks + lh) ^ sw) * 8;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[buf][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bfr[buf][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
+  };
+  // Residual chunk of (i, j, part): EP 0 / 1: 4 channels at column
+  // 32 j + 8 part + 4 lh (part = g, 0..3); EP 2: 8 channels at column
+  // 32 j + 16 part + 8 lh (part 0..1).  Row 32 i + lane % 32 of the block.
+  constexpr int NPART = EP == 2 ? 2 : 4;
+  using ResT = typename std::conditional<EP == 2, uint4, uint2>::type;
+  int q = 0;
+  for (int tile = t_lo; tile < t_hi; ++tile) {
+    const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+    const int mw = m0 + wm * TM * 32, nw = n0 + wn * kWC;  // origin of this wave's block
+    ResT rr[TM][TN][NPART];
+    if (res) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int p = 0; p < NPART; ++p) {
+            const int m = mw + 32 * i + lrow;
+            const int n = nw + 32 * j + (EP == 2 ? 16 * p + 8 * lh : 8 * p + 4 * lh);
+            if (m < a.M && n < a.N) rr[i][j][p] = *reinterpret_cast<const ResT *>(res + (int64_t)m * a.ldr + n);
+            else if constexpr (EP == 2) rr[i][j][p] = make_uint4(0u, 0u, 0u, 0u);
+            else rr[i][j][p] = make_uint2(0u, 0u);
+          }
+    }
+    // acc[i][j][4 g + e] = C[mw + 32 i + lrow][nw + 32 j + 8 g + 4 lh + e]
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    for (int kt = 0; kt < nk; ++kt, ++q) {
+      __builtin_amdgcn_s_barrier();
+      const uint16_t *S = smem + (q % STAGES) * kStage;
+      read_frags(S, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      static_for<KS>([&](auto ksc) {
+        constexpr int ks = decltype(ksc)::value;
+        constexpr int cur = ks & 1;
+        if constexpr (ks + 1 < KS) read_frags(S, ks + 1, cur ^ 1);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
+        sched_step<0, TM * TN, (ks + 1 < KS) ? TM + TN : 0, 0>();
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
+    // Epilogue: bias, residual, activation and one rounding per element.
+    if constexpr (EP == 2) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int m = mw + 32 * i + lrow;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int p = 0; p < 2; ++p) {
+            // Lower half-wave keeps group 2p and receives the upper half's
+            // group 2p; the upper half receives the lower half's group 2p + 1.
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][8 * p + e]),
+                                                                __float_as_uint(acc[i][j][8 * p + 4 + e]), false, false);
+              v[e] = __uint_as_float(sw2[0]);
+              v[4 + e] = __uint_as_float(sw2[1]);
+            }
+            const int n = nw + 32 * j + 16 * p + 8 * lh;
+            if (n < a.N) {
+              if (bias_lds || a.bias) {
+                const float *bsrc = bias_lds ? bias_s + n : a.bias + n;
+                const float4 b0 = *reinterpret_cast<const float4 *>(bsrc);
+                const float4 b1 = *reinterpret_cast<const float4 *>(bsrc + 4);
+                v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+                v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+              }
+              if (res) {
+                const uint4 rv = rr[i][j][p];
+                const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  v[2 * e] += bf2f((uint16_t)(w4[e] & 0xffff));
+                  v[2 * e + 1] += bf2f((uint16_t)(w4[e] >> 16));
+                }
+              }
+              uint32_t o[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                o[e] = f2bf(epilogue_act(v[2 * e], a.relu, a.gelu)) |
+                       ((uint32_t)f2bf(epilogue_act(v[2 * e + 1], a.relu, a.gelu)) << 16);
+              if (m < a.M) *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+            }
+          }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int m = mw + 32 * i + lrow;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int col = 32 * j + 8 * g + 4 * lh, n = nw + col;
+            const float4 bv = n >= a.N ? make_float4(0.f, 0.f, 0.f, 0.f)
+                              : bias_lds ? *reinterpret_cast<const float4 *>(bias_s + n)
+                              : a.bias   ? *reinterpret_cast<const float4 *>(a.bias + n)
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+            float v[4] = {acc[i][j][4 * g] + bv.x, acc[i][j][4 * g + 1] + bv.y, acc[i][j][4 * g + 2] + bv.z,
+                          acc[i][j][4 * g + 3] + bv.w};
+            if (res) {
+              const uint2 rv = *reinterpret_cast<const uint2 *>(&rr[i][j][g]);
+              v[0] += bf2f((uint16_t)(rv.x & 0xffff));
+              v[1] += bf2f((uint16_t)(rv.x >> 16));
+              v[2] += bf2f((uint16_t)(rv.y & 0xffff));
+              v[3] += bf2f((uint16_t)(rv.y >> 16));
+            }
+            uint2 o;
+            o.x = f2bf(epilogue_act(v[0], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[1], a.relu, a.gelu)) << 16);
+            o.y = f2bf(epilogue_act(v[2], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[3], a.relu, a.gelu)) << 16);
+            if (EP == 1) *reinterpret_cast<uint2 *>(slab + lrow * kEP + col) = o;
+            else if (m < a.M && n < a.N) *reinterpret_cast<uint2 *>(y + (int64_t)m * a.ldc + n) = o;
+          }
+        if (EP == 1) {
+          // The slab is private to this wave: order its writes before the
+          // reads of other lanes, then store row segments of kWC columns.
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          constexpr int CPR = kWC / 8;  // 16-byte chunks per slab row
+#pragma unroll
+          for (int c = lane; c < 32 * CPR; c += 64) {
+            const int row = c / CPR, col = (c % CPR) * 8;
+            const int mm = mw + 32 * i + row, n = nw + col;
+            const uint4 val = *reinterpret_cast<const uint4 *>(slab + row * kEP + col);
+            if (mm < a.M && n < a.N) *reinterpret_cast<uint4 *>(y + (int64_t)mm * a.ldc + n) = val;
+          }
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
+      }
+    }
+  }
+}
+
+// CUs of the current device (persistent grids use one workgroup per CU).
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] <= 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cached[dev] = v;
+  }
+  return cached[dev];
+}
+
+template <int BM, int BN, int WM, int WN, int PW, int STAGES, int LD, int KW, int EP>
+hipError_t launch_pws_cfg(const ConvArgs &a, hipStream_t s) {
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const int grid = tiles < cu_count() ? tiles : cu_count();
+  hipLaunchKernelGGL((conv_bf16_pws_kernel<BM, BN, WM, WN, PW, STAGES, LD, KW, EP>), dim3(grid),
+                     dim3((WM * WN + PW) * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int PW, int STAGES, int LD, int EP>
+hipError_t launch_pws_ld(const ConvArgs &a, hipStream_t s) {
+  if ((LD == LD_NHWC || LD == LD_CAT) && a.kh == 3)
+    return launch_pws_cfg<BM, BN, WM, WN, PW, STAGES, LD, 3, EP>(a, s);
+  return launch_pws_cfg<BM, BN, WM, WN, PW, STAGES, LD, 1, EP>(a, s);
+}
+
 // ------------------------------------------- bf16, streaming 1 x 1 kernel
 //
 // For 1 x 1 convolutions with short K (the memory-bound ResNet layers) the
@@ -1270,17 +1598,46 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     case 23: return launch_ws_ld<256, 64, 4, 1, 4, LD, 0, 1>(a, s);
     case 24: return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
     case 25: return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+    case 40: return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 1>(a, s);
+    case 41: return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
+    case 42: return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
+    case 43: return launch_pws_ld<256, 128, 4, 2, 2, 3, LD, 2>(a, s);
+    case 44: return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 2>(a, s);
+    case 45: return launch_pws_ld<256, 64, 4, 1, 4, 3, LD, 2>(a, s);
+    case 46: return launch_pws_ld<256, 64, 8, 1, 4, 3, LD, 2>(a, s);
+    case 47: return launch_pws_ld<256, 128, 4, 2, 4, 2, LD, 2>(a, s);
     default: break;
   }
-  // Measured on MI355X over the ResNet-50 conv shapes.  With at least two
-  // k-tiles the warp-specialised kernel (two workgroups per CU) wins; for a
-  // single k-tile its extra synchronisation does not pay.  For 64-channel
-  // outputs with short K the three-stage pipelined kernel stays ahead.
-  if (a.K >= 2 * BK && ws_eligible(a, (Loader)LD)) {
+  // Measured on MI355X over the ResNet-50 conv shapes (per-layer kernel
+  // traces of every configuration above):
+  // - the warp-specialised kernel with two workgroups per CU (128 x 64 tiles)
+  //   for the space-to-depth stem, 64-channel outputs with K = 64 or K >= 512,
+  //   and residual layers with >= 1024 output channels; with 128 x 128 tiles
+  //   for the other residual layers and for 128-channel outputs with K > 256;
+  // - the persistent kernel (one workgroup of 8 consumer and 4 producer waves
+  //   per CU) with 128 x 256 tiles for the fused shortcut GEMMs and the other
+  //   layers, and with 256 x 128 tiles for 128-channel 1 x 1 layers with short
+  //   K and for >= 512 channels with K >= 2048;
+  // - the three-stage pipelined kernel for single k-tiles (and 64-channel
+  //   outputs with K = 128 .. 448), where warp specialisation does not pay.
+  if (ws_eligible(a, (Loader)LD)) {
+    if (LD == LD_S2D) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
     if (a.N <= 64) {
-      if (a.K >= 512) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
-    } else {
-      return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+      if (a.K >= 512 || a.K == BK) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+    } else if (a.res) {
+      if (a.K >= 2 * BK) {
+        if (a.N >= 1024) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+        return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+      }
+    } else if (LD == LD_CAT) {
+      return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
+    } else if (a.N <= 128) {
+      if (a.kh == 1 && a.K <= 256 && a.K >= 2 * BK) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
+      if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+    } else if (a.N >= 512 && a.K >= 2048) {
+      return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
+    } else if (a.K >= 2 * BK) {
+      return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
     }
   }
   if (a.N <= 64) {
