@@ -453,12 +453,24 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
   } else {
     ld = (cs.k == 1 && cs.stride == 1 && cs.pad == 0) ? LD_GEMM : LD_NHWC;
   }
-  const double flops = 2.0 * a.M * (double)a.N * a.K;
+  const double flops = 2.0 * a.M * (double)a.N * (cs.s2d ? (double)cs.cin * cs.k * cs.k : (double)a.K);
   const double bytes = (double)c.m.esz * ((double)nb * in.elems() + (double)a.M * a.N * (res ? 2 : 1) +
                                           (double)a.N * a.K + (cs.fused ? (double)a.M * cs.cin2 : 0.0));
   if (c.m.bf16)
     return timed(c.s, F_CONV_BF16, flops, bytes, [&] { return launch_conv_bf16(a, ld, c.s); });
   return timed(c.s, F_CONV_F32, flops, bytes, [&] { return launch_conv_f32(a, ld, c.s); });
+}
+
+// A ResNet stem (7 x 7 stride-2 convolution with ReLU on space-to-depth
+// cells, 64 channels) followed by 3 x 3 stride-2 max pooling with padding 1.
+bool stem_pool_fusable(const Model &m) {
+  if (!m.bf16 || m.layers.size() < 2 || !m.first_reads_nchw) return false;
+  const LayerPlan &l0 = m.layers[0], &l1 = m.layers[1];
+  if (l0.L.kind != HAPI_CONV || l0.convs.empty() || !l0.convs[0].s2d || !l0.L.relu) return false;
+  const ConvSpec &cs = l0.convs[0];
+  if (cs.k != 7 || cs.stride != 2 || cs.pad != 3 || cs.Kp != 4 * 4 * kS2DChannels) return false;
+  if (l1.L.kind != HAPI_MAXPOOL || l1.L.k != 3 || l1.L.stride != 2 || l1.L.pad != 1) return false;
+  return stem_pool_supported(l0.in.c, l0.in.h, l0.in.w, cs.cout, l0.out.h, l0.out.w, l1.out.h, l1.out.w);
 }
 
 // Runs layers 1..split on nb images; writes the split output (caller layout)
@@ -480,7 +492,25 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
     cur = c.slot[0];
     cur_slot = 0;
   }
-  for (int li = 0; li < split; ++li) {
+  int li0 = 0;
+  // Stem convolution and max pooling in one kernel when the stem output is
+  // not itself the split and layers are not being timed one by one.
+  if (split >= 2 && !c.on_layer && stem_pool_fusable(m) && (uintptr_t)images % 4 == 0) {
+    const LayerPlan &l0 = m.layers[0], &l1 = m.layers[1];
+    const ConvSpec &cs = l0.convs[0];
+    const int o = free_slot();
+    const double flops = 2.0 * nb * l0.out.h * l0.out.w * (double)cs.cout * cs.cin * cs.k * cs.k;
+    const double bytes = (double)m.esz * ((double)nb * (l0.in.elems() + l1.out.elems()) + (double)cs.cout * cs.Kp);
+    HIP_TRY(timed(c.s, F_CONV_BF16, flops, bytes, [&] {
+      return launch_stem_pool_bf16(images, c.pk + cs.pk_w, cs.Kp, reinterpret_cast<const float *>(c.pk + cs.pk_b),
+                                   c.slot[o], nb, l0.in.c, l0.in.h, l0.in.w, l0.out.h, l0.out.w, l1.out.h,
+                                   l1.out.w, c.s);
+    }));
+    cur = c.slot[o];
+    cur_slot = o;
+    li0 = 2;
+  }
+  for (int li = li0; li < split; ++li) {
     const LayerPlan &lp = m.layers[li];
     const hapi_layer &L = lp.L;
     if (c.on_layer) c.on_layer(li, true);

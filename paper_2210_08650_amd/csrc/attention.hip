@@ -18,12 +18,6 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
 
 template <int TP>
 __global__ __launch_bounds__(256) void attention_kernel(const uint16_t *__restrict__ qkv,
@@ -140,8 +134,8 @@ __global__ __launch_bounds__(256) void attention_kernel(const uint16_t *__restri
         for (int g = 0; g < 4; ++g) {
           const int d0 = 32 * db + 8 * g + 4 * hl;
           uint2 w;
-          w.x = f2bf(o[db][4 * g] * inv) | ((uint32_t)f2bf(o[db][4 * g + 1] * inv) << 16);
-          w.y = f2bf(o[db][4 * g + 2] * inv) | ((uint32_t)f2bf(o[db][4 * g + 3] * inv) << 16);
+          w.x = f2bf2(o[db][4 * g] * inv, o[db][4 * g + 1] * inv);
+          w.y = f2bf2(o[db][4 * g + 2] * inv, o[db][4 * g + 3] * inv);
           *reinterpret_cast<uint2 *>(orow + d0) = w;
         }
     }

@@ -39,12 +39,6 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
 
 __device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float((uint32_t)u << 16); }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
-  u += 0x7fffu + ((u >> 16) & 1u);                      // round to nearest even
-  return (uint16_t)(u >> 16);
-}
 
 __device__ __forceinline__ float epilogue_act(float v, int relu, int gelu) {
   if (relu) v = fmaxf(v, 0.0f);
@@ -581,8 +575,8 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
             v[3] += bf2f((uint16_t)(rv.y >> 16));
           }
           uint2 o;
-          o.x = f2bf(epilogue_act(v[0], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[1], a.relu, a.gelu)) << 16);
-          o.y = f2bf(epilogue_act(v[2], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[3], a.relu, a.gelu)) << 16);
+          o.x = f2bf2(epilogue_act(v[0], a.relu, a.gelu), epilogue_act(v[1], a.relu, a.gelu));
+          o.y = f2bf2(epilogue_act(v[2], a.relu, a.gelu), epilogue_act(v[3], a.relu, a.gelu));
           *reinterpret_cast<uint2 *>(y + (int64_t)m * a.ldc + n) = o;
         }
       }
@@ -634,7 +628,7 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     for (int e = 0; e < 4; ++e) {
       const float lo = epilogue_act(v[2 * e] + bias[2 * e], a.relu, a.gelu);
       const float hi = epilogue_act(v[2 * e + 1] + bias[2 * e + 1], a.relu, a.gelu);
-      o[e] = f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+      o[e] = f2bf2(lo, hi);
     }
     *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
   }
@@ -907,8 +901,8 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
             v[3] += bf2f((uint16_t)(rv.y >> 16));
           }
           uint2 o;
-          o.x = f2bf(epilogue_act(v[0], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[1], a.relu, a.gelu)) << 16);
-          o.y = f2bf(epilogue_act(v[2], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[3], a.relu, a.gelu)) << 16);
+          o.x = f2bf2(epilogue_act(v[0], a.relu, a.gelu), epilogue_act(v[1], a.relu, a.gelu));
+          o.y = f2bf2(epilogue_act(v[2], a.relu, a.gelu), epilogue_act(v[3], a.relu, a.gelu));
           *reinterpret_cast<uint2 *>(y + (int64_t)m * a.ldc + n) = o;
         }
       }
@@ -963,7 +957,7 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
     for (int e = 0; e < 4; ++e) {
       const float lo = epilogue_act(v[2 * e] + bias[2 * e], a.relu, a.gelu);
       const float hi = epilogue_act(v[2 * e + 1] + bias[2 * e + 1], a.relu, a.gelu);
-      o[e] = f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+      o[e] = f2bf2(lo, hi);
     }
     *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
   }
@@ -1248,8 +1242,7 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
               uint32_t o[4];
 #pragma unroll
               for (int e = 0; e < 4; ++e)
-                o[e] = f2bf(epilogue_act(v[2 * e], a.relu, a.gelu)) |
-                       ((uint32_t)f2bf(epilogue_act(v[2 * e + 1], a.relu, a.gelu)) << 16);
+                o[e] = f2bf2(epilogue_act(v[2 * e], a.relu, a.gelu), epilogue_act(v[2 * e + 1], a.relu, a.gelu));
               if (m < a.M) *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
             }
           }
@@ -1277,8 +1270,8 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
               v[3] += bf2f((uint16_t)(rv.y >> 16));
             }
             uint2 o;
-            o.x = f2bf(epilogue_act(v[0], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[1], a.relu, a.gelu)) << 16);
-            o.y = f2bf(epilogue_act(v[2], a.relu, a.gelu)) | ((uint32_t)f2bf(epilogue_act(v[3], a.relu, a.gelu)) << 16);
+            o.x = f2bf2(epilogue_act(v[0], a.relu, a.gelu), epilogue_act(v[1], a.relu, a.gelu));
+            o.y = f2bf2(epilogue_act(v[2], a.relu, a.gelu), epilogue_act(v[3], a.relu, a.gelu));
             if (EP == 1) *reinterpret_cast<uint2 *>(slab + lrow * kEP + col) = o;
             else if (m < a.M && n < a.N) *reinterpret_cast<uint2 *>(y + (int64_t)m * a.ldc + n) = o;
           }
@@ -1515,8 +1508,7 @@ __global__ __launch_bounds__(2 * WM * WN * 64) void conv_bf16_stream_kernel(Conv
       uint32_t o[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        o[e] = f2bf(epilogue_act(v[2 * e], a.relu, a.gelu)) |
-               ((uint32_t)f2bf(epilogue_act(v[2 * e + 1], a.relu, a.gelu)) << 16);
+        o[e] = f2bf2(epilogue_act(v[2 * e], a.relu, a.gelu), epilogue_act(v[2 * e + 1], a.relu, a.gelu));
       *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

@@ -11,12 +11,6 @@ namespace {
 
 __device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float((uint32_t)u << 16); }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
 
 inline int blocks_for(int64_t n, int per_block) { return (int)((n + per_block - 1) / per_block); }
 
@@ -75,10 +69,10 @@ __global__ void maxpool_kernel(const T *__restrict__ x, T *__restrict__ y, int n
   const int64_t ob = (((int64_t)img * Ho + ho) * Wo + wo) * C + g * 8;
   if constexpr (sizeof(T) == 2) {
     uint4 q;
-    q.x = f2bf(m[0]) | ((uint32_t)f2bf(m[1]) << 16);
-    q.y = f2bf(m[2]) | ((uint32_t)f2bf(m[3]) << 16);
-    q.z = f2bf(m[4]) | ((uint32_t)f2bf(m[5]) << 16);
-    q.w = f2bf(m[6]) | ((uint32_t)f2bf(m[7]) << 16);
+    q.x = f2bf2(m[0], m[1]);
+    q.y = f2bf2(m[2], m[3]);
+    q.z = f2bf2(m[4], m[5]);
+    q.w = f2bf2(m[6], m[7]);
     *reinterpret_cast<uint4 *>(y + ob) = q;
   } else {
     *reinterpret_cast<float4 *>(y + ob) = make_float4(m[0], m[1], m[2], m[3]);
@@ -189,10 +183,10 @@ __global__ void tokens_kernel(const uint16_t *__restrict__ patch, const float *_
 #pragma unroll
   for (int j = 0; j < 8; ++j) v[j] += pos[(int64_t)tok * D + g * 8 + j];
   uint4 o;
-  o.x = f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-  o.y = f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-  o.z = f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-  o.w = f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+  o.x = f2bf2(v[0], v[1]);
+  o.y = f2bf2(v[2], v[3]);
+  o.z = f2bf2(v[4], v[5]);
+  o.w = f2bf2(v[6], v[7]);
   *reinterpret_cast<uint4 *>(y + row * D + g * 8) = o;
 }
 
@@ -365,7 +359,7 @@ __global__ void affine_relu_kernel(const uint16_t *__restrict__ x, const float *
     const int c = g * 8 + 2 * j;
     const float lo = fmaxf(bf2f((uint16_t)(w4[j] & 0xffff)) * scale[c] + shift[c], 0.0f);
     const float hi = fmaxf(bf2f((uint16_t)(w4[j] >> 16)) * scale[c + 1] + shift[c + 1], 0.0f);
-    o[j] = f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+    o[j] = f2bf2(lo, hi);
   }
   *reinterpret_cast<uint4 *>(y + p * C + g * 8) = make_uint4(o[0], o[1], o[2], o[3]);
 }

@@ -9,6 +9,17 @@
 
 namespace hapi {
 
+// bfloat16 from float32 on the device, rounded to nearest even
+// (v_cvt_pk_bf16_f32: identical to integer RNE on every finite value,
+// denormals included; a NaN stays a NaN).  f2bf2 packs (lo, hi) into one word.
+typedef __bf16 bf16x2_dev_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_dev_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  const f32x2_dev_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_dev_t));
+}
+
 // ---------------------------------------------------------------- kernels
 
 // Where a convolution reads its input from.
@@ -87,6 +98,13 @@ hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, c
 hipError_t launch_space_to_depth(const void *x, void *y, int n, int C, int H, int W, int pad,
                                  int HP, int WP, hipStream_t s);
 constexpr int kS2DChannels = 16;
+// Fused ResNet stem: 7 x 7 stride-2 pad-3 convolution on space-to-depth cells
+// (packed weights [64][ldw] in PACK_S2D order, float32 bias, ReLU, one bf16
+// rounding) and 3 x 3 stride-2 pad-1 max pooling, from NCHW bf16 images to the
+// pooled NHWC output [n, Hp, Wp, 64].  bf16 only; see stem_pool_supported.
+bool stem_pool_supported(int C, int H, int W, int cout, int Ho, int Wo, int Hp, int Wp);
+hipError_t launch_stem_pool_bf16(const void *x, const void *w, int ldw, const float *bias, void *y, int n, int C,
+                                 int H, int W, int Ho, int Wo, int Hp, int Wp, hipStream_t s);
 hipError_t launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s);
 // Channel-slice copy (concatenation): y[p * cy + off + c] = x[p * cx + c], c < C,
 // for `pixels` NHWC pixels.  C, cx, cy, off multiples of 8.  bf16.

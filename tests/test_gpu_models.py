@@ -7,6 +7,7 @@ accumulation, one rounding per materialised tensor).  Batch partitioning
 (storage-side batch adaptation) must not change a single bit.
 """
 import numpy as np
+import torch
 import pytest
 
 import paper_2210_08650_amd as H
@@ -163,8 +164,34 @@ def test_kernel_stats_count_launches():
     r.extract(xd, 18)
     st = {s["name"]: s for s in H.hapi_stats_collect()}
     H.hapi_stats_enable(False)
-    # stem + 16 blocks x 3 convs; the 4 projection shortcuts join their
-    # block's last convolution
+    # stem with its max pooling + 16 blocks x 3 convs; the 4 projection
+    # shortcuts join their block's last convolution
     assert st["conv_bf16"]["launches"] == 1 + 48
     assert st["conv_bf16"]["total_ms"] > 0 and st["conv_bf16"]["flops"] > 0
-    assert st["maxpool"]["launches"] == 1
+    assert "maxpool" not in st
+    # the stem output itself as the split: stem and pooling run separately
+    H.hapi_stats_enable(True)
+    r.extract(xd, 1)
+    st = {s["name"]: s for s in H.hapi_stats_collect()}
+    H.hapi_stats_enable(False)
+    assert st["conv_bf16"]["launches"] == 1 and "maxpool" not in st
+    H.hapi_stats_enable(True)
+    r.extract(xd, 3)
+    st = {s["name"]: s for s in H.hapi_stats_collect()}
+    H.hapi_stats_enable(False)
+    assert st["conv_bf16"]["launches"] == 1 + 3 and "maxpool" not in st
+
+
+@pytest.mark.parametrize("name", ["resnet18", "resnet50", "densenet_block"])
+def test_fused_stem_pool_is_bit_exact(name):
+    """With the split past the max pooling, the stem convolution and the
+    pooling run as one kernel; its output must equal, bit for bit, the stem
+    output (split 1) pooled by the library's own max-pooling layer."""
+    r, _, _, xd, _, dtype = _setup(name, 50, 3)
+    fused = r.extract(xd, 2)
+    stem = r.extract(xd, 1)
+    pool = Runner([PM.maxpool(3, 2, 1)], dtype, [], tuple(stem.shape[1:]))
+    ref = pool.extract(stem.contiguous(), 1)
+    print(f"{name}: fused {tuple(fused.shape)} vs stem + pool {tuple(ref.shape)}", flush=True)
+    assert fused.shape == ref.shape
+    assert torch.equal(fused, ref)
