@@ -1848,6 +1848,10 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
     // The pipelined kernel needs 16-byte output rows; the register-staged one
     // handles element gathers (NCHW stems) and any other width.
     case LD_NHWC:
+      if (!a.gelu && a.Ho == a.H && a.Wo == a.W && forced_cfg() < 0 &&
+          conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
+        return launch_conv3x3_c64(a.x, a.w, a.Kp, a.bias, a.res, a.ldr, a.y, a.ldc, a.n_img, a.H, a.W, a.relu != 0,
+                                  cu_count(), s);
       return (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) ? launch_pipe_ld<LD_NHWC>(a, s)
                                                                  : launch_bf16_ld<LD_NHWC>(a, s);
     case LD_GEMM:

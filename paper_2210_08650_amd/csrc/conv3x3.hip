@@ -1,0 +1,253 @@
+// Row-streaming 3 x 3 convolution for gfx950: stride 1, padding 1, 64 input
+// and 64 output channels, NHWC bf16, image width <= 64 (the ResNet stage-1
+// bottleneck and basic-block convolutions).
+//
+// The implicit-GEMM kernels gather every k-tile of such a layer from L2 (each
+// input pixel is fetched nine times, once per tap) and are bound by the
+// latency of that traffic.  Here a workgroup (one per CU) keeps the whole
+// weight matrix [64][576] in LDS and streams the input rows of one image band
+// through a ring of LDS rows, so every input element moves from HBM to LDS
+// once.  Each step computes four output rows, each split over two waves (32
+// pixels x 64 channels, 36 k-steps of 2 MFMAs; two waves per SIMD) while the
+// next four input rows load.
+//
+// Reduction order: k = (kh, kw, c) in sequence, 16 channels per MFMA step, as
+// in the implicit-GEMM kernels.  The MFMA operands are swapped (weights as A)
+// so a lane's accumulators hold 4 consecutive channels of one pixel; half-wave
+// exchanges give each lane 8 consecutive channels, stored as 16-byte chunks
+// after bias, optional residual, ReLU and one rounding.
+#include <cstdint>
+#include <type_traits>
+#include <utility>
+
+#include "internal.h"
+
+namespace hapi {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kC = 64;                 // input and output channels
+constexpr int kK = 9 * kC;             // 576
+constexpr int kWPitch = kK + 8;        // bf16 pitch of a weight row in LDS (conflict-free fragment reads)
+constexpr int kPix = 66;               // pixels per ring row: columns -1 .. 64
+constexpr int kRows = 10;              // ring rows: a step reads 6, the next 4 are loading
+constexpr int kStepRows = 4;           // output rows per step
+constexpr int kWaves = 2 * kStepRows;  // two waves per row: 32-pixel halves
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRowChunks = kPix * 8;   // 16-byte chunks per ring row
+
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// Calls f(integral_constant<int, i>) for i = 0 .. N-1 (compile-time indices).
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Chunk c (8 channels) of pixel slot p sits at chunk c ^ ((p >> 1) & 7): the
+// 16 pixels a quarter-wave reads land in 16 distinct bank groups.
+__device__ __forceinline__ int ring_off(int slot, int p, int c) { return (slot * kPix + p) * kC + ((c ^ ((p >> 1) & 7)) << 3); }
+
+struct Conv3Args {
+  const uint16_t *x;    // [n, H, W, 64]
+  const uint16_t *w;    // packed [64][ldw], k = (kh, kw, c)
+  const float *bias;    // [64] or null
+  const uint16_t *res;  // [n * H * W][ldr] or null
+  uint16_t *y;          // [n * H * W][ldc]
+  int H, W, ldw, ldc, ldr, relu;
+  int bands, band_rows;  // output rows [b * band_rows, ...) of each image per workgroup
+};
+
+__global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
+  __shared__ __attribute__((aligned(16))) uint16_t wts[kC * kWPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t ring[kRows * kPix * kC];
+  __shared__ float bias_s[kC];
+
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int lrow = lane & 31, lh = lane >> 5;
+  const int img = blockIdx.x / a.bands, band = blockIdx.x - img * a.bands;
+  const int r0 = band * a.band_rows;
+  const int r1 = min(a.H, r0 + a.band_rows);
+  const int64_t img_px = (int64_t)img * a.H * a.W;
+
+  // Input row h (-1 .. H) lives in ring slot (h + 1) % kRows; outside the
+  // image and in the padding columns it is zero.  Item it moves 16 bytes.
+  // Branch-free: a chunk outside the image reads the image's first pixel and
+  // is zeroed when stored, so the loads of a whole row set stay in flight.
+  auto load_row = [&](int h, int it) -> uint4 {
+    const int p = it >> 3, c = it & 7;  // ring pixel p holds column p - 1
+    const int col = p - 1;
+    const bool ok = it < kRowChunks && (unsigned)h < (unsigned)a.H && (unsigned)col < (unsigned)a.W;
+    const int64_t pix = ok ? (int64_t)h * a.W + col : 0;
+    uint4 v = *reinterpret_cast<const uint4 *>(a.x + ((img_px + pix) << 6) + c * 8);
+    if (!ok) v = make_uint4(0u, 0u, 0u, 0u);
+    return v;
+  };
+  constexpr int kPer = (kRowChunks + kThreads - 1) / kThreads;  // chunks per thread per row
+  auto store_row = [&](int h, int it, const uint4 &v) {
+    const int p = it >> 3, c = it & 7;
+    *reinterpret_cast<uint4 *>(ring + ring_off((h + 1) % kRows, p, c)) = v;
+  };
+
+  // Prologue: every load (weights and the first six input rows) is issued
+  // before any store, so their latencies overlap.
+  {
+    constexpr int kWPer = kC * (kK / 8) / kThreads;  // chunks of 16 bytes
+    uint4 wv[kWPer];
+    uint4 iv[6][kPer];
+#pragma unroll
+    for (int e = 0; e < kWPer; ++e) {
+      const int i = t + e * kThreads, n = i / (kK / 8), k8 = i - n * (kK / 8);
+      wv[e] = *reinterpret_cast<const uint4 *>(a.w + (int64_t)n * a.ldw + k8 * 8);
+    }
+#pragma unroll
+    for (int q = 0; q < 6; ++q)
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) iv[q][e] = load_row(r0 - 1 + q, t + e * kThreads);
+#pragma unroll
+    for (int e = 0; e < kWPer; ++e) {
+      const int i = t + e * kThreads, n = i / (kK / 8), k8 = i - n * (kK / 8);
+      *reinterpret_cast<uint4 *>(wts + n * kWPitch + k8 * 8) = wv[e];
+    }
+#pragma unroll
+    for (int q = 0; q < 6; ++q)
+#pragma unroll
+      for (int e = 0; e < kPer; ++e)
+        if (t + e * kThreads < kRowChunks) store_row(r0 - 1 + q, t + e * kThreads, iv[q][e]);
+  }
+  if (t < kC) bias_s[t] = a.bias ? a.bias[t] : 0.0f;
+  __syncthreads();
+
+  // Fragment offsets: A (weights) row n = 32 j + lane % 32 at k = 16 s + 8 lh;
+  // B (activations) pixel 32 i + lane % 32 (+ kw) at channel chunk 2 cs + lh.
+  const int aoff0 = lrow * kWPitch + 8 * lh, aoff1 = (32 + lrow) * kWPitch + 8 * lh;
+  uint16_t *y = a.y;
+
+  for (int ho = r0; ho < r1; ho += kStepRows) {
+    // The input rows of the next step load while this one computes.
+    uint4 pre[4][kPer];
+    const bool more = ho + kStepRows < r1;
+    if (more) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+          pre[q][e] = load_row(ho + 5 + q, t + e * kThreads);
+        }
+    }
+    const int row = ho + (wave & (kStepRows - 1));  // this wave's output row
+    const int pi = wave / kStepRows;                 // and its 32-pixel half
+    f32x16_t acc[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[j][e] = 0.0f;
+    if (row < r1) {
+      // Fragments are read kAhead k-steps before their MFMAs (a ring of
+      // kAhead + 1 register sets), so the LDS latency hides behind 2 kAhead
+      // MFMAs of this wave plus those of the other wave on the SIMD.
+      constexpr int kSteps = 36, kAhead = 3, kSlots = kAhead + 1;
+      int slot_base[3];
+#pragma unroll
+      for (int kh = 0; kh < 3; ++kh) slot_base[kh] = ((row + kh) % kRows) * kPix * kC;
+      bf16x8_t fw0[kSlots], fw1[kSlots], fx[kSlots];
+      auto read_step = [&](int st, int sl) {
+        const int kh = st / 12, kw = (st / 4) % 3, cs = st % 4;
+        fw0[sl] = *reinterpret_cast<const bf16x8_t *>(wts + aoff0 + 16 * st);
+        fw1[sl] = *reinterpret_cast<const bf16x8_t *>(wts + aoff1 + 16 * st);
+        const int p = 32 * pi + lrow + kw;
+        fx[sl] = *reinterpret_cast<const bf16x8_t *>(ring + slot_base[kh] + p * kC + (((2 * cs + lh) ^ ((p >> 1) & 7)) << 3));
+      };
+      static_for<kAhead>([&](auto sc) { read_step(decltype(sc)::value, decltype(sc)::value); });
+      static_for<kSteps>([&](auto sc) {
+        constexpr int st = decltype(sc)::value, sl = st % kSlots;
+        if constexpr (st + kAhead < kSteps) read_step(st + kAhead, (st + kAhead) % kSlots);
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw0[sl], fx[sl], acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw1[sl], fx[sl], acc[1], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      // acc[j][4 g + e] = channel 32 j + 8 g + 4 lh + e of pixel 32 pi + lane % 32.
+      // After the half-wave exchange of part q, a lane owns channels
+      // 32 j + 16 q + 8 lh .. + 8 of that pixel.
+      {
+        const int px = 32 * pi + lrow;
+        const int64_t m = img_px + (int64_t)row * a.W + px;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[j][8 * q + e]),
+                                                               __float_as_uint(acc[j][8 * q + 4 + e]), false, false);
+              v[e] = __uint_as_float(sw[0]);
+              v[4 + e] = __uint_as_float(sw[1]);
+            }
+            const int n = 32 * j + 16 * q + 8 * lh;
+            const float4 b0 = *reinterpret_cast<const float4 *>(bias_s + n);
+            const float4 b1 = *reinterpret_cast<const float4 *>(bias_s + n + 4);
+            v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+            v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+            if (px < a.W) {
+              if (a.res) {
+                const uint4 rv = *reinterpret_cast<const uint4 *>(a.res + m * a.ldr + n);
+                const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  v[2 * e] += __uint_as_float(w4[e] << 16);
+                  v[2 * e + 1] += __uint_as_float(w4[e] & 0xffff0000u);
+                }
+              }
+              uint32_t o[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                o[e] = a.relu ? f2bf2(fmaxf(v[2 * e], 0.0f), fmaxf(v[2 * e + 1], 0.0f)) : f2bf2(v[2 * e], v[2 * e + 1]);
+              *reinterpret_cast<uint4 *>(y + m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+            }
+          }
+      }
+    }
+    if (more) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+          const int it = t + e * kThreads;
+          if (it < kRowChunks) store_row(ho + 5 + q, it, pre[q][e]);
+        }
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, int W, int Kp, int ldc, int ldr) {
+  return C == kC && N == kC && kh == 3 && kw == 3 && stride == 1 && pad == 1 && W >= 1 && W <= kPix - 2 &&
+         Kp == kK && ldc % 8 == 0 && ldr % 8 == 0;
+}
+
+hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float *bias, const void *res, int ldr,
+                              void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s) {
+  // Enough workgroups to fill the CUs: split images into bands of rows.
+  int bands = (cus + n - 1) / n;
+  bands = bands < 1 ? 1 : bands;
+  const int max_bands = (H + kStepRows - 1) / kStepRows;
+  bands = bands > max_bands ? max_bands : bands;
+  int band_rows = (H + bands - 1) / bands;
+  band_rows = (band_rows + kStepRows - 1) / kStepRows * kStepRows;
+  bands = (H + band_rows - 1) / band_rows;
+  Conv3Args a{static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(w), bias,
+              static_cast<const uint16_t *>(res), static_cast<uint16_t *>(y), H, W, ldw, ldc, ldr, relu ? 1 : 0,
+              bands, band_rows};
+  hipLaunchKernelGGL(conv3x3_c64_kernel, dim3(n * bands), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace hapi

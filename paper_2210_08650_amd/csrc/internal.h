@@ -102,6 +102,13 @@ constexpr int kS2DChannels = 16;
 // (packed weights [64][ldw] in PACK_S2D order, float32 bias, ReLU, one bf16
 // rounding) and 3 x 3 stride-2 pad-1 max pooling, from NCHW bf16 images to the
 // pooled NHWC output [n, Hp, Wp, 64].  bf16 only; see stem_pool_supported.
+// Row-streaming 3 x 3 stride-1 pad-1 convolution with 64 input and output
+// channels (NHWC bf16, width <= 64): weights resident in LDS, input rows
+// streamed once.  k = (kh, kw, c), packed [64][ldw]; optional residual;
+// cus = CUs to fill.
+bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, int W, int Kp, int ldc, int ldr);
+hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float *bias, const void *res, int ldr,
+                              void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s);
 bool stem_pool_supported(int C, int H, int W, int cout, int Ho, int Wo, int Hp, int Wp);
 hipError_t launch_stem_pool_bf16(const void *x, const void *w, int ldw, const float *bias, void *y, int n, int C,
                                  int H, int W, int Ho, int Wo, int Hp, int Wp, hipStream_t s);
