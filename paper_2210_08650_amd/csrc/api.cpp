@@ -352,6 +352,15 @@ int64_t workspace_for(const Model &m, int split, int chunk, bool profile, int ba
 
 // ------------------------------------------------------------- kernel stats
 
+}  // namespace
+
+LaunchEvents &launch_events() {
+  static thread_local LaunchEvents e;
+  return e;
+}
+
+namespace {
+
 enum Family { F_CONV_BF16, F_CONV_F32, F_ATTN, F_LN, F_MAXPOOL, F_AVGPOOL, F_TOKENS, F_LAYOUT,
               F_COPY, F_AFFINE, F_COUNT };
 const char *kFamily[F_COUNT] = {"conv_bf16", "conv_f32", "attention", "layernorm", "maxpool",
@@ -382,12 +391,20 @@ hipEvent_t take_event() {
 template <class F>
 hipError_t timed(hipStream_t s, int fam, double flops, double bytes, F &&launch) {
   if (!g_stats_on) return launch();
+  (void)s;
   std::lock_guard<std::mutex> g(g_stats_mu);
   hipEvent_t a = take_event(), b = take_event();
-  if (a) (void)hipEventRecord(a, s);
+  // The launch records a and b as part of its dispatch (hapi_launch).
+  if (a && b) launch_events() = LaunchEvents{a, b};
   hipError_t r = launch();
-  if (b) (void)hipEventRecord(b, s);
-  if (a && b) g_recs.push_back(StatRec{fam, a, b, flops, bytes});
+  const bool used = launch_events().start == nullptr;
+  launch_events() = LaunchEvents{};
+  if (a && b && used && r == hipSuccess) {
+    g_recs.push_back(StatRec{fam, a, b, flops, bytes});
+  } else {
+    if (a) g_pool.push_back(a);
+    if (b) g_pool.push_back(b);
+  }
   return r;
 }
 

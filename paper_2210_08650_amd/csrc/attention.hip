@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256) void attention_kernel(const uint16_t *__restri
 template <int TP>
 hipError_t launch_tp(const void *qkv, void *out, int n, int T, int D, int heads, hipStream_t s) {
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)kHeadDim);
-  hipLaunchKernelGGL(attention_kernel<TP>, dim3(n * heads), dim3(256), 0, s,
+  hapi_launch(attention_kernel<TP>, dim3(n * heads), dim3(256), 0, s,
                      (const uint16_t *)qkv, (uint16_t *)out, T, D, heads, scale_log2);
   return hipGetLastError();
 }

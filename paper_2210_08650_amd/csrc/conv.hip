@@ -977,10 +977,10 @@ template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 
 hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if constexpr (MINB >= 2)
-    hipLaunchKernelGGL((conv_bf16_ws2_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
+    hapi_launch((conv_bf16_ws2_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
                        dim3(2 * WM * WN * 64), 0, s, a);
   else
-    hipLaunchKernelGGL((conv_bf16_ws_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
+    hapi_launch((conv_bf16_ws_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
                        dim3(2 * WM * WN * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -988,14 +988,14 @@ hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
 template <int BM, int BN, int LD>
 hipError_t launch_bf16_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((conv_bf16_kernel<BM, BN, LD>), dim3(tiles), dim3(kThreads), 0, s, a);
+  hapi_launch((conv_bf16_kernel<BM, BN, LD>), dim3(tiles), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
 template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED = 1, int EPI = 0>
 hipError_t launch_pipe_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED, EPI>), dim3(tiles),
+  hapi_launch((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED, EPI>), dim3(tiles),
                      dim3(WM * WN * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -1315,7 +1315,7 @@ template <int BM, int BN, int WM, int WN, int PW, int STAGES, int LD, int KW, in
 hipError_t launch_pws_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   const int grid = tiles < cu_count() ? tiles : cu_count();
-  hipLaunchKernelGGL((conv_bf16_pws_kernel<BM, BN, WM, WN, PW, STAGES, LD, KW, EP>), dim3(grid),
+  hapi_launch((conv_bf16_pws_kernel<BM, BN, WM, WN, PW, STAGES, LD, KW, EP>), dim3(grid),
                      dim3((WM * WN + PW) * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -1521,7 +1521,7 @@ template <int BM, int BN, int WM, int WN, int STAGES, int LD>
 hipError_t launch_stream_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = (a.M + BM - 1) / BM;
   const int grid = tiles < kStreamWorkgroups ? tiles : kStreamWorkgroups;
-  hipLaunchKernelGGL((conv_bf16_stream_kernel<BM, BN, WM, WN, STAGES, LD>), dim3(grid), dim3(2 * WM * WN * 64), 0,
+  hapi_launch((conv_bf16_stream_kernel<BM, BN, WM, WN, STAGES, LD>), dim3(grid), dim3(2 * WM * WN * 64), 0,
                      s, a);
   return hipGetLastError();
 }
@@ -1807,7 +1807,7 @@ __global__ __launch_bounds__(kThreads) void conv_f32_kernel(ConvArgs a) {
 template <int BM, int BN, int LD>
 hipError_t launch_f32_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((conv_f32_kernel<BM, BN, LD>), dim3(tiles), dim3(kThreads), 0, s, a);
+  hapi_launch((conv_f32_kernel<BM, BN, LD>), dim3(tiles), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -246,7 +246,7 @@ hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float
   Conv3Args a{static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(w), bias,
               static_cast<const uint16_t *>(res), static_cast<uint16_t *>(y), H, W, ldw, ldc, ldr, relu ? 1 : 0,
               bands, band_rows};
-  hipLaunchKernelGGL(conv3x3_c64_kernel, dim3(n * bands), dim3(kThreads), 0, s, a);
+  hapi_launch(conv3x3_c64_kernel, dim3(n * bands), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

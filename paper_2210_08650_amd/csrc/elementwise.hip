@@ -378,7 +378,7 @@ __global__ void pack_affine_kernel(const float *__restrict__ bn, int C, float *_
 hipError_t launch_channel_copy(const void *x, void *y, int64_t pixels, int C, int cx, int cy,
                                int off, hipStream_t s) {
   const int64_t total = pixels * (C / 8);
-  hipLaunchKernelGGL(channel_copy_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+  hapi_launch(channel_copy_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                      (const uint16_t *)x, (uint16_t *)y, pixels, C, cx, cy, off);
   return hipGetLastError();
 }
@@ -386,13 +386,13 @@ hipError_t launch_channel_copy(const void *x, void *y, int64_t pixels, int C, in
 hipError_t launch_affine_relu(const void *x, const float *scale, const float *shift, void *y,
                               int64_t pixels, int C, int cx, hipStream_t s) {
   const int64_t total = pixels * (C / 8);
-  hipLaunchKernelGGL(affine_relu_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+  hapi_launch(affine_relu_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                      (const uint16_t *)x, scale, shift, (uint16_t *)y, pixels, C, cx);
   return hipGetLastError();
 }
 
 hipError_t launch_pack_affine(const float *bn, int C, float *scale, float *shift, hipStream_t s) {
-  hipLaunchKernelGGL(pack_affine_kernel, dim3(blocks_for(C, 256)), dim3(256), 0, s, bn, C, scale,
+  hapi_launch(pack_affine_kernel, dim3(blocks_for(C, 256)), dim3(256), 0, s, bn, C, scale,
                      shift);
   return hipGetLastError();
 }
@@ -400,7 +400,7 @@ hipError_t launch_pack_affine(const float *bn, int C, float *scale, float *shift
 hipError_t launch_space_to_depth(const void *x, void *y, int n, int C, int H, int W, int pad,
                                  int HP, int WP, hipStream_t s) {
   const int64_t total = (int64_t)n * HP * WP;
-  hipLaunchKernelGGL(s2d_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+  hapi_launch(s2d_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                      (const uint16_t *)x, (uint16_t *)y, n, C, H, W, pad, HP, WP);
   return hipGetLastError();
 }
@@ -409,10 +409,10 @@ hipError_t launch_maxpool(bool bf16, const void *x, void *y, int n, int H, int W
                           int stride, int pad, int Ho, int Wo, hipStream_t s) {
   const int64_t total = (int64_t)n * Ho * Wo * (C / 8);
   if (bf16)
-    hipLaunchKernelGGL(maxpool_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+    hapi_launch(maxpool_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                        (const uint16_t *)x, (uint16_t *)y, n, H, W, C, k, stride, pad, Ho, Wo);
   else
-    hipLaunchKernelGGL(maxpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+    hapi_launch(maxpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                        (const float *)x, (float *)y, n, H, W, C, k, stride, pad, Ho, Wo);
   return hipGetLastError();
 }
@@ -421,10 +421,10 @@ hipError_t launch_avgpool(bool bf16, const void *x, void *y, int n, int H, int W
                           int stride, int Ho, int Wo, hipStream_t s) {
   const int64_t total = (int64_t)n * Ho * Wo * C;
   if (bf16)
-    hipLaunchKernelGGL(avgpool_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+    hapi_launch(avgpool_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                        (const uint16_t *)x, (uint16_t *)y, n, H, W, C, k, stride, Ho, Wo);
   else
-    hipLaunchKernelGGL(avgpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+    hapi_launch(avgpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                        (const float *)x, (float *)y, n, H, W, C, k, stride, Ho, Wo);
   return hipGetLastError();
 }
@@ -433,10 +433,10 @@ static hipError_t launch_transpose(bool bf16, const void *x, void *y, int n, int
                                    hipStream_t s) {
   const dim3 grid((S + 63) / 64, (R + 63) / 64, n);
   if (bf16)
-    hipLaunchKernelGGL(transpose_kernel<uint16_t>, grid, dim3(256), 0, s, (const uint16_t *)x,
+    hapi_launch(transpose_kernel<uint16_t>, grid, dim3(256), 0, s, (const uint16_t *)x,
                        (uint16_t *)y, R, S);
   else
-    hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, (const float *)x,
+    hapi_launch(transpose_kernel<float>, grid, dim3(256), 0, s, (const float *)x,
                        (float *)y, R, S);
   return hipGetLastError();
 }
@@ -456,9 +456,9 @@ hipError_t launch_copy(const void *x, void *y, size_t bytes, hipStream_t s) {
   if (((uintptr_t)x % 16) == 0 && ((uintptr_t)y % 16) == 0 && bytes % 16 == 0) {
     const int64_t n16 = (int64_t)(bytes / 16);
     const int blocks = (int)std::min<int64_t>(blocks_for(n16, 256), 8192);
-    hipLaunchKernelGGL(copy16_kernel, dim3(blocks), dim3(256), 0, s, (const uint4 *)x, (uint4 *)y, n16);
+    hapi_launch(copy16_kernel, dim3(blocks), dim3(256), 0, s, (const uint4 *)x, (uint4 *)y, n16);
   } else {
-    hipLaunchKernelGGL(copy1_kernel, dim3(blocks_for((int64_t)bytes, 256)), dim3(256), 0, s,
+    hapi_launch(copy1_kernel, dim3(blocks_for((int64_t)bytes, 256)), dim3(256), 0, s,
                        (const uint8_t *)x, (uint8_t *)y, (int64_t)bytes);
   }
   return hipGetLastError();
@@ -466,7 +466,7 @@ hipError_t launch_copy(const void *x, void *y, size_t bytes, hipStream_t s) {
 
 hipError_t launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(copy_f32_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, x, y, n);
+  hapi_launch(copy_f32_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, x, y, n);
   return hipGetLastError();
 }
 
@@ -474,10 +474,10 @@ hipError_t launch_fill_pattern(bool bf16, void *y, int64_t n, uint32_t seed, flo
                                hipStream_t s) {
   if (n == 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(fill_kernel<uint16_t>, dim3(blocks_for(n, 256)), dim3(256), 0, s,
+    hapi_launch(fill_kernel<uint16_t>, dim3(blocks_for(n, 256)), dim3(256), 0, s,
                        (uint16_t *)y, n, seed, scale);
   else
-    hipLaunchKernelGGL(fill_kernel<float>, dim3(blocks_for(n, 256)), dim3(256), 0, s, (float *)y,
+    hapi_launch(fill_kernel<float>, dim3(blocks_for(n, 256)), dim3(256), 0, s, (float *)y,
                        n, seed, scale);
   return hipGetLastError();
 }
@@ -485,14 +485,14 @@ hipError_t launch_fill_pattern(bool bf16, void *y, int64_t n, uint32_t seed, flo
 hipError_t launch_tokens(const void *patch, const float *cls, const float *pos, void *y, int n,
                          int T, int D, hipStream_t s) {
   const int64_t total = (int64_t)n * T * (D / 8);
-  hipLaunchKernelGGL(tokens_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+  hapi_launch(tokens_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                      (const uint16_t *)patch, cls, pos, (uint16_t *)y, n, T, D);
   return hipGetLastError();
 }
 
 hipError_t launch_layernorm(const void *x, const float *gamma, const float *beta, void *y,
                             int64_t rows, int D, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(layernorm_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
+  hapi_launch(layernorm_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
                      (const uint16_t *)x, gamma, beta, (uint16_t *)y, rows, D, eps);
   return hipGetLastError();
 }
@@ -503,11 +503,11 @@ hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, c
                             PackOrder order, void *wp, float *bias_out, hipStream_t s) {
   const int64_t total = (int64_t)N * kcols;
   if (bf16)
-    hipLaunchKernelGGL(pack_conv_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+    hapi_launch(pack_conv_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                        w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, kcols, ldw, koff,
                        (int)acc_bias, (int)order, (uint16_t *)wp, bias_out);
   else
-    hipLaunchKernelGGL(pack_conv_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+    hapi_launch(pack_conv_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                        w, conv_bias, gamma, beta, mean, var, N, C, kh, kw, kcols, ldw, koff,
                        (int)acc_bias, (int)order, (float *)wp, bias_out);
   return hipGetLastError();

@@ -1,6 +1,7 @@
 // Internal declarations shared by the host runtime and the HIP kernels of libhapi.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -18,6 +19,25 @@ __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(ui
 __device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
   const f32x2_dev_t v = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_dev_t));
+}
+
+// ---------------------------------------------------------------- launches
+
+// Timing events for the next kernel launch of this thread (kernel
+// statistics).  When set, the launch records them at the start and the end of
+// the dispatch itself, so the measured time is the kernel's own duration.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents &launch_events();
+
+// Every kernel of the library is launched through here.
+template <typename F, typename... Args>
+inline void hapi_launch(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  LaunchEvents &e = launch_events();
+  hipEvent_t a = e.start, b = e.stop;
+  e.start = e.stop = nullptr;
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, a, b, 0u, args...);
 }
 
 // ---------------------------------------------------------------- kernels

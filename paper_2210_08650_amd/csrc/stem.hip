@@ -254,7 +254,7 @@ hipError_t launch_stem_pool_bf16(const void *x, const void *w, int ldw, const fl
                                  int H, int W, int Ho, int Wo, int Hp, int Wp, hipStream_t s) {
   StemArgs a{static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(w), bias, static_cast<uint16_t *>(y),
              n, C, H, W, ldw, Ho, Wo, Hp, Wp};
-  hipLaunchKernelGGL(stem_pool_kernel, dim3(2 * n), dim3(64 * kStemWaves), 0, s, a);
+  hapi_launch(stem_pool_kernel, dim3(2 * n), dim3(64 * kStemWaves), 0, s, a);
   return hipGetLastError();
 }
 
