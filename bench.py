@@ -23,6 +23,8 @@ import time
 import numpy as np
 
 PEAK = {"bf16": 2500.0, "f32": 157.3}  # dense MFMA TFLOP/s (MI355X)
+# Sources of the convolution kernel family whose counters the traffic profile holds.
+CONV_SOURCES = ("conv.hip", "conv3x3.hip", "stem.hip")
 HBM_PEAK = 8000.0                      # GB/s
 
 
@@ -37,15 +39,17 @@ def _cores():
 
 def measured_traffic(workload):
     """HBM bytes per convolution launch from the committed rocprofv3 counter
-    summary, or None when the convolution source changed since it was taken."""
+    summary, or None when a convolution source changed since it was taken."""
     import hashlib
     root = os.path.dirname(os.path.abspath(__file__))
     path = os.path.join(root, "profiles", "conv_bf16_resnet50_b256_hbm_traffic.md")
     if workload != "resnet50_bf16_b256" or not os.path.exists(path):
         return None
     kv = dict(line.strip().split("=", 1) for line in open(path) if "=" in line and " " not in line.strip())
-    src = os.path.join(root, "paper_2210_08650_amd", "csrc", "conv.hip")
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != kv.get("conv_source_sha256"):
+    h = hashlib.sha256()
+    for name in CONV_SOURCES:
+        h.update(open(os.path.join(root, "paper_2210_08650_amd", "csrc", name), "rb").read())
+    if h.hexdigest() != kv.get("conv_source_sha256"):
         return None
     return float(kv["conv_traffic_bytes_per_launch"])
 
