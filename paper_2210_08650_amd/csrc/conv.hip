@@ -1298,6 +1298,151 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
   }
 }
 
+// ------------------------------------- bf16, short-K (one or two k-tiles)
+//
+// For GEMMs with K <= 128 (the memory-bound 1 x 1 layers) a tile's whole
+// A and B fit in LDS, and the time per tile is one memory round trip, which
+// under load is several microseconds.  Each workgroup issues all of its loads
+// at once (the k-tiles by LDS DMA, its residual block into registers, its
+// bias slice into LDS), waits once, runs the MFMAs and stores 16-byte chunks
+// after a half-wave exchange (as the persistent kernel's epilogue).  Several
+// workgroups per CU at different phases keep the loads of the whole device in
+// flight.
+template <int BM, int BN, int WM, int WN, int KT, int LD, int MINB>
+__global__ __launch_bounds__(WM * WN * 64, MINB) void conv_bf16_short_kernel(ConvArgs a) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / (WM * 32), TN = BN / (WN * 32);
+  constexpr int NA = BM * 8 / NT, NB = BN * 8 / NT;  // DMA instructions per thread per k-tile
+  constexpr int KS = BK / 16;
+  constexpr int kStage = (BM + BN) * BK;
+  constexpr int kWC = TN * 32;
+  static_assert(TM >= 1 && TN >= 1 && NA >= 1 && NB >= 1 && KT >= 1 && KT <= 2, "tile");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[KT * kStage];
+  __shared__ __attribute__((aligned(16))) float bias_s[BN];
+
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int lrow = lane & 31, lh = lane >> 5;
+  const int mw = m0 + wm * TM * 32, nw = n0 + wn * kWC;  // this wave's block
+
+  // All loads first: the k-tiles (LDS DMA), then the residual block and the
+  // bias slice into registers; one wait covers them all.
+  DmaPlan<NA, NB, LD> dp;
+  dp.init(a, m0, n0, wave * NA, wave * NB, lane);
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    uint16_t *As = smem + kt * kStage;
+    dp.issue(a, kt, As, As + BM * BK, 0, NA + NB);
+  }
+  // Residual chunks of (i, j, part): 8 channels at column 32 j + 16 part + 8 lh
+  // of row 32 i + lane % 32 of the block.
+  uint4 rr[TM][TN][2];
+  const uint16_t *res = static_cast<const uint16_t *>(a.res);
+  if (res) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const int m = mw + 32 * i + lrow, n = nw + 32 * j + 16 * p + 8 * lh;
+          rr[i][j][p] = (m < a.M && n < a.N) ? *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n)
+                                             : make_uint4(0u, 0u, 0u, 0u);
+        }
+  }
+  const float bv = (t < BN && a.bias && n0 + t < a.N) ? a.bias[n0 + t] : 0.0f;
+  wait_vmcnt<0>();  // every load of this tile (the DMAs, the residual, the bias)
+  if (t < BN) bias_s[t] = bv;
+  __syncthreads();
+
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) aoff[i] = (wm * TM * 32 + i * 32 + lrow) * BK;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) boff[j] = BM * BK + (wn * kWC + j * 32 + lrow) * BK;
+  const int sw = (lrow >> 1) & 7;
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    const uint16_t *S = smem + kt * kStage;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int ch = ((2 * ks + lh) ^ sw) * 8;
+      bf16x8_t af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+    }
+  }
+  uint16_t *y = static_cast<uint16_t *>(a.y);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = mw + 32 * i + lrow;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][8 * p + e]),
+                                                            __float_as_uint(acc[i][j][8 * p + 4 + e]), false, false);
+          v[e] = __uint_as_float(sw2[0]);
+          v[4 + e] = __uint_as_float(sw2[1]);
+        }
+        const int nl = wn * kWC + 32 * j + 16 * p + 8 * lh, n = n0 + nl;
+        if (n < a.N && m < a.M) {
+          const float4 b0 = *reinterpret_cast<const float4 *>(bias_s + nl);
+          const float4 b1 = *reinterpret_cast<const float4 *>(bias_s + nl + 4);
+          v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+          v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+          if (res) {
+            const uint4 rv = rr[i][j][p];
+            const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] += bf2f((uint16_t)(w4[e] & 0xffff));
+              v[2 * e + 1] += bf2f((uint16_t)(w4[e] >> 16));
+            }
+          }
+          uint32_t o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            o[e] = f2bf2(epilogue_act(v[2 * e], a.relu, a.gelu), epilogue_act(v[2 * e + 1], a.relu, a.gelu));
+          *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+      }
+  }
+}
+
+template <int BM, int BN, int WM, int WN, int KT, int LD, int MINB>
+hipError_t launch_short_cfg(const ConvArgs &a, hipStream_t s) {
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  hapi_launch((conv_bf16_short_kernel<BM, BN, WM, WN, KT, LD, MINB>), dim3(tiles), dim3(WM * WN * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int LD, int MINB>
+hipError_t launch_short_ld(const ConvArgs &a, hipStream_t s) {
+  if (a.Kp == 2 * BK) return launch_short_cfg<BM, BN, WM, WN, 2, LD, MINB>(a, s);
+  return launch_short_cfg<BM, BN, WM, WN, 1, LD, MINB>(a, s);
+}
+
 // CUs of the current device (persistent grids use one workgroup per CU).
 int cu_count() {
   static int cached[64] = {0};
@@ -1598,6 +1743,11 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     case 45: return launch_pws_ld<256, 64, 4, 1, 4, 3, LD, 2>(a, s);
     case 46: return launch_pws_ld<256, 64, 8, 1, 4, 3, LD, 2>(a, s);
     case 47: return launch_pws_ld<256, 128, 4, 2, 4, 2, LD, 2>(a, s);
+    case 50: if (a.Kp <= 2 * BK) return launch_short_ld<128, 128, 2, 2, LD, 3>(a, s); break;
+    case 51: if (a.Kp <= 2 * BK) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s); break;
+    case 52: if (a.Kp <= 2 * BK) return launch_short_ld<64, 128, 2, 2, LD, 4>(a, s); break;
+    case 53: if (a.Kp <= 2 * BK) return launch_short_ld<128, 256, 2, 4, LD, 2>(a, s); break;
+    case 54: if (a.Kp <= 2 * BK) return launch_short_ld<64, 64, 2, 2, LD, 4>(a, s); break;
     default: break;
   }
   // Measured on MI355X over the ResNet-50 conv shapes (per-layer kernel
@@ -1610,8 +1760,13 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
   //   per CU) with 128 x 256 tiles for the fused shortcut GEMMs and the other
   //   layers, and with 256 x 128 tiles for 128-channel 1 x 1 layers with short
   //   K and for >= 512 channels with K >= 2048;
-  // - the three-stage pipelined kernel for single k-tiles (and 64-channel
+  // - the three-stage pipelined kernel for other single k-tiles (and 64-channel
   //   outputs with K = 128 .. 448), where warp specialisation does not pay.
+  // Single k-tile 64-channel 1 x 1 layers and 512-channel residual 1 x 1
+  // layers with two k-tiles: all loads of a tile at once, several workgroups
+  // per CU (short-K kernel).
+  if (LD == LD_GEMM && a.Kp == BK && a.N <= 64 && !a.res) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s);
+  if (LD == LD_GEMM && a.Kp == 2 * BK && a.N == 512 && a.res) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s);
   if (ws_eligible(a, (Loader)LD)) {
     if (LD == LD_S2D) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
     if (a.N <= 64) {
