@@ -13,8 +13,10 @@
  *
  * Conventions shared by every entry point
  *  - Every data pointer is a DEVICE pointer owned by the caller (allocate with
- *    hipMalloc or as torch tensors).  The library never allocates or frees
- *    device memory except a few hipEvents for timing.
+ *    hipMalloc or as torch tensors), except the host arrays of
+ *    hapi_layer_shape, hapi_profile_layers, hapi_stats_collect and
+ *    hapi_choose_split.  The library never allocates or frees device memory
+ *    except a few hipEvents for timing.
  *  - Return value: HAPI_OK (0) or a negative hapi_status.  The message of the
  *    last failure on the calling thread is returned by hapi_last_error().
  *    Every argument is validated before anything is launched, so a call that
@@ -51,7 +53,8 @@ typedef enum {
   HAPI_OK = 0,
   HAPI_E_INVAL = -1,       /* bad argument: null pointer, split out of range, bad shape */
   HAPI_E_UNSUPPORTED = -2, /* a layer kind / dtype / shape combination not built */
-  HAPI_E_NOMEM = -3,       /* workspace smaller than hapi_workspace_bytes() requires */
+  HAPI_E_NOMEM = -3,       /* workspace smaller than hapi_workspace_bytes() requires;
+                              hapi_choose_split: even the freeze split would OOM */
   HAPI_E_DEVICE = -4       /* a HIP call or kernel launch failed */
 } hapi_status;
 
@@ -218,6 +221,97 @@ typedef struct {
 
 int hapi_stats_enable(int32_t enable);
 int hapi_stats_collect(hapi_kernel_stat *out, int32_t max_entries);
+
+/* ---------------------------------------------------------------------------
+ * Split-index choice (Algorithm 1 and its competitors, Evaluation,
+ * Methodology).  Pure host arithmetic over the profile above plus the
+ * caller's client-side and environment measurements; no device access, works
+ * without a GPU.  Times in seconds, sizes in bytes.
+ *
+ * Per-iteration estimates for a split s (phases of Table 1; "Profiling and
+ * modeling runtime"):
+ *   requests  R = train_batch / request_images, waves V = ceil(R / server_slots)
+ *   RT_SRV(s) = V * [read_data + read_model + to_gpu
+ *                    + request_images * image_bytes[s] * (from_gpu + pickle)]
+ *               + R * sum_{k=1..s} srv_layer_s[k]
+ *     (the forward passes of concurrent requests serialise on the GPU, every
+ *     other phase runs in parallel, and a request waits for the wave of
+ *     requests in front of it).  At s = 0 the server runs no layer: only
+ *     read_data and pickle remain.
+ *   RT_NW(s)  = train_batch * image_bytes[s] / net_bytes_per_s
+ *   RT_CLI(s) = train_batch * image_bytes[s] * (unpickle + loader + cli_to_gpu)
+ *               + sum_{k=s+1..n_layers} cli_layer_s[k] + cli_rest_s
+ *   memory(s) = cli_fixed_mem_bytes + train_batch * max(image_bytes[s],
+ *               max_{k=s+1..n_layers} (image_bytes[k-1] + image_bytes[k]))
+ *     (Design, "Memory usage estimation": the peak of the forward pass is the
+ *     layer with the largest input + output); s is predicted to OOM when
+ *     cli_mem_bytes > 0 and memory(s) > cli_mem_bytes.
+ *   epoch(s)  = RT_SRV + max(RT_SRV + RT_NW, RT_CLI) * (iterations - 1) + RT_CLI
+ *     (Algorithm 1: the client's work overlaps the server's work and the
+ *     transfer of the next iteration).  When nosplit_iter_s > 0, split 0 uses
+ *     iterations * nosplit_iter_s instead: its per-iteration time was measured
+ *     while profiling the earliest split (Design, notes after Algorithm 1).
+ * Sums over layers run in ascending k; argmins take the earliest index on ties.
+ */
+typedef struct {
+  int32_t n_layers;           /* layers of the profiled model, >= 1 */
+  int32_t freeze_idx;         /* user's freeze index, 0..n_layers */
+  int32_t train_batch;        /* training batch size (images per iteration), >= 1 */
+  int32_t request_images;     /* images per POST request (paper: 128); divides train_batch */
+  int32_t server_slots;       /* requests the server runs at once (paper: 4), >= 1 */
+  int32_t reserved0;          /* must be 0 */
+  int64_t iterations;         /* NR_IT: iterations per epoch, >= 1 */
+  const int64_t *image_bytes; /* [n_layers+1] host: layer-k output bytes of ONE image
+                                 (hapi_profile_layers at batch 1), each >= 1 */
+  const double *srv_layer_s;  /* [n_layers+1] host: server forward time of layer k for one
+                                 request (hapi_profile_layers out_us at batch
+                                 request_images, in seconds); [0] is ignored */
+  const double *cli_layer_s;  /* [n_layers+1] host: client forward time of layer k at the
+                                 training batch; [0] is ignored */
+  double srv_read_data_s;     /* per request: read its objects from storage */
+  double srv_read_model_s;    /* per request: load the model to the GPU (0 with reuse) */
+  double srv_to_gpu_s;        /* per request: move its input to the GPU */
+  double cli_rest_s;          /* per iteration: split-independent client work (layers after
+                                 the profiled ones, backward pass, optimiser step) */
+  double srv_from_gpu_s_per_byte; /* linear phases, seconds per byte of split output */
+  double srv_pickle_s_per_byte;
+  double cli_unpickle_s_per_byte;
+  double cli_loader_s_per_byte;
+  double cli_to_gpu_s_per_byte;
+  double net_bytes_per_s;     /* network bandwidth, > 0 */
+  int64_t cli_mem_bytes;      /* client GPU memory; 0 = never predict an OOM */
+  int64_t cli_fixed_mem_bytes;/* split-independent client memory (weights, optimiser,
+                                 training activations) */
+  double nosplit_iter_s;      /* measured per-iteration time at split 0, or <= 0 */
+} hapi_split_job;
+
+typedef struct {
+  double rt_srv, rt_nw, rt_cli; /* per-iteration estimates */
+  double epoch_s;               /* Algorithm 1's epoch runtime estimate */
+  double sum_s;                 /* RT_SRV + RT_NW + RT_CLI (NSG's objective) */
+  int64_t cli_mem_bytes;        /* client memory estimate */
+  int32_t oom;                  /* 1 = predicted to run out of client memory */
+  int32_t reserved;
+} hapi_split_estimate;
+
+typedef struct {
+  int32_t hapi;       /* Algorithm 1: argmin epoch_s over non-OOM splits in [0, freeze_idx] */
+  int32_t earliest;   /* earliest non-OOM split (profiled in the second half of epoch 0) */
+  int32_t freeze;     /* @Freeze: freeze_idx */
+  int32_t min_output; /* @Min: smallest image_bytes[k] over k = 1..freeze_idx, earliest
+                         on ties (0 when freeze_idx = 0); may be predicted to OOM */
+  int32_t nosplit;    /* NoSplit: 0; may be predicted to OOM */
+  int32_t nsg;        /* NSG: argmin sum_s over non-OOM splits in [0, freeze_idx] */
+} hapi_split_choice;
+
+/* Fills `choice` and, if `est` is not NULL, est[s] for s = 0..freeze_idx (host
+ * arrays owned by the caller).  Errors: HAPI_E_INVAL (NULL pointer, a count or
+ * index out of range, a negative or non-finite time or rate, train_batch not
+ * a multiple of request_images, a byte count that overflows), HAPI_E_NOMEM
+ * (the freeze split itself is predicted to OOM: so is every other split,
+ * Algorithm 1's first step).  On error nothing is written. */
+int hapi_choose_split(const hapi_split_job *job, hapi_split_estimate *est,
+                      hapi_split_choice *choice);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *hapi_last_error(void);

@@ -8,6 +8,7 @@ the only module both sides use is ``synth`` (seeded random inputs).
 ``layers`` wraps the plain-C float64 layer definitions in ``oracle.c``;
 ``models`` assembles them into the frozen feature extractors the paper splits
 (Measurement study; Evaluation, Table 2) and runs the forward pass from the
-input up to a split layer (Design, "Request flow"; System implementation).
+input up to a split layer (Design, "Request flow"; System implementation);
+``split`` is Algorithm 1's split-index choice and its competitors.
 """
-from . import layers, models  # noqa: F401
+from . import layers, models, split  # noqa: F401

@@ -27,7 +27,8 @@ __all__ = ["HapiError", "Desc", "hapi_layer", "hapi_model_desc", "hapi_kernel_st
            "HAPI_VIT_BLOCK", "HAPI_LAYERNORM", "HAPI_DENSE_BLOCK", "LIB_PATH", "EXPORTED",
            "hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
            "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-           "hapi_profile_layers", "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error"]
+           "hapi_profile_layers", "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error",
+           "hapi_split_job", "hapi_split_estimate", "hapi_split_choice", "hapi_choose_split"]
 
 _STATUS = {HAPI_E_INVAL: "HAPI_E_INVAL", HAPI_E_UNSUPPORTED: "HAPI_E_UNSUPPORTED",
            HAPI_E_NOMEM: "HAPI_E_NOMEM", HAPI_E_DEVICE: "HAPI_E_DEVICE"}
@@ -59,6 +60,39 @@ class hapi_kernel_stat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
                 ("bytes", ctypes.c_double)]
+
+
+class hapi_split_job(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("freeze_idx", ctypes.c_int32),
+                ("train_batch", ctypes.c_int32), ("request_images", ctypes.c_int32),
+                ("server_slots", ctypes.c_int32), ("reserved0", ctypes.c_int32),
+                ("iterations", ctypes.c_int64),
+                ("image_bytes", ctypes.POINTER(ctypes.c_int64)),
+                ("srv_layer_s", ctypes.POINTER(ctypes.c_double)),
+                ("cli_layer_s", ctypes.POINTER(ctypes.c_double)),
+                ("srv_read_data_s", ctypes.c_double), ("srv_read_model_s", ctypes.c_double),
+                ("srv_to_gpu_s", ctypes.c_double), ("cli_rest_s", ctypes.c_double),
+                ("srv_from_gpu_s_per_byte", ctypes.c_double),
+                ("srv_pickle_s_per_byte", ctypes.c_double),
+                ("cli_unpickle_s_per_byte", ctypes.c_double),
+                ("cli_loader_s_per_byte", ctypes.c_double),
+                ("cli_to_gpu_s_per_byte", ctypes.c_double),
+                ("net_bytes_per_s", ctypes.c_double),
+                ("cli_mem_bytes", ctypes.c_int64), ("cli_fixed_mem_bytes", ctypes.c_int64),
+                ("nosplit_iter_s", ctypes.c_double)]
+
+
+class hapi_split_estimate(ctypes.Structure):
+    _fields_ = [("rt_srv", ctypes.c_double), ("rt_nw", ctypes.c_double),
+                ("rt_cli", ctypes.c_double), ("epoch_s", ctypes.c_double),
+                ("sum_s", ctypes.c_double), ("cli_mem_bytes", ctypes.c_int64),
+                ("oom", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class hapi_split_choice(ctypes.Structure):
+    _fields_ = [("hapi", ctypes.c_int32), ("earliest", ctypes.c_int32),
+                ("freeze", ctypes.c_int32), ("min_output", ctypes.c_int32),
+                ("nosplit", ctypes.c_int32), ("nsg", ctypes.c_int32)]
 
 
 def _hip_runtimes():
@@ -95,6 +129,9 @@ def _load():
         "hapi_stats_enable": (ctypes.c_int, [i32]),
         "hapi_stats_collect": (ctypes.c_int, [ctypes.POINTER(hapi_kernel_stat), i32]),
         "hapi_last_error": (ctypes.c_char_p, []),
+        "hapi_choose_split": (ctypes.c_int, [ctypes.POINTER(hapi_split_job),
+                                             ctypes.POINTER(hapi_split_estimate),
+                                             ctypes.POINTER(hapi_split_choice)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -105,7 +142,8 @@ def _load():
 _lib = _load()
 EXPORTED = ("hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
             "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-            "hapi_profile_layers", "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error")
+            "hapi_profile_layers", "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error",
+            "hapi_choose_split")
 
 
 def _ptr(p):
@@ -225,3 +263,34 @@ def hapi_stats_collect(max_entries: int = 16) -> list:
 def hapi_last_error() -> str:
     msg = _lib.hapi_last_error()
     return msg.decode() if msg else ""
+
+
+_SPLIT_ARRAYS = {"image_bytes": ctypes.c_int64, "srv_layer_s": ctypes.c_double,
+                 "cli_layer_s": ctypes.c_double}
+
+
+def hapi_choose_split(**job):
+    """Fields of ``hapi_split_job`` as keywords (the three per-layer arrays as
+    sequences of ``n_layers + 1`` values).  Returns ``(choice, estimates)``:
+    a dict of the ``hapi_split_choice`` fields and one dict of
+    ``hapi_split_estimate`` fields per split 0..freeze_idx."""
+    j = hapi_split_job()
+    keep = []
+    for key, val in job.items():
+        if key in _SPLIT_ARRAYS:
+            if len(val) != int(job.get("n_layers", 0)) + 1:
+                raise ValueError(f"{key} must hold n_layers + 1 values, got {len(val)}")
+            arr = (_SPLIT_ARRAYS[key] * len(val))(*val)
+            keep.append(arr)
+            setattr(j, key, ctypes.cast(arr, ctypes.POINTER(_SPLIT_ARRAYS[key])))
+        else:
+            setattr(j, key, val)
+    nf = max(int(j.freeze_idx), 0) + 1
+    est = (hapi_split_estimate * nf)()
+    ch = hapi_split_choice()
+    _check(_lib.hapi_choose_split(ctypes.byref(j), est, ctypes.byref(ch)))
+    choice = {name: int(getattr(ch, name)) for name, _ in hapi_split_choice._fields_}
+    rows = [{name: (int(v) if isinstance(v, int) else float(v))
+             for name, v in ((f, getattr(est[s], f)) for f, _ in hapi_split_estimate._fields_)
+             if name != "reserved"} for s in range(nf)]
+    return choice, rows

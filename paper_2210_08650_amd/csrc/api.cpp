@@ -14,7 +14,6 @@
 #include "internal.h"
 
 namespace hapi {
-namespace {
 
 // ------------------------------------------------------------------ errors
 
@@ -29,6 +28,8 @@ int fail(int code, const char *fmt, ...) {
   g_err = buf;
   return code;
 }
+
+namespace {
 
 #define HIP_TRY(expr)                                                                  \
   do {                                                                                 \

@@ -31,6 +31,9 @@ struct LaunchEvents {
 };
 LaunchEvents &launch_events();
 
+// Records a printf-style message for hapi_last_error() and returns `code`.
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+
 // Every kernel of the library is launched through here.
 template <typename F, typename... Args>
 inline void hapi_launch(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {

@@ -109,3 +109,40 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     """Widen bfloat16 bit patterns (uint16) to the float32 values they encode."""
     b = np.ascontiguousarray(bits, np.uint16).astype(np.uint32) << 16
     return b.view(np.float32)
+
+
+def split_job(workload: int, image_bytes, freeze_idx: int, train_batch: int = 512,
+              request_images: int = 128, server_slots: int = 4,
+              images_per_epoch: int = 30720) -> dict:
+    """Random split-choice job (field names of the library's split-job record).
+
+    Stand-in measurements for the paper's setting (Evaluation, Methodology):
+    requests of 128 objects, at most 4 run at once, an epoch of 30720 images
+    and a 12 Gbps network, with every time and throughput drawn uniformly
+    around plausible values: per-layer forward times of 0.2-5 ms per request
+    on the server and 0.5-20 ms per training batch on the client, reading a
+    request 20-80 ms, loading the model 50-300 ms, copies at 10-25 GB/s,
+    (un)pickling at 1-4 GB/s, data loading at 2-8 GB/s, the bandwidth scaled
+    by 0.25-4x.  ``image_bytes`` (the per-image output sizes) is passed in.
+    """
+    rng = _rng(workload, 900)
+    n = len(image_bytes) - 1
+    layer = lambda lo, hi: [0.0] + [float(v) for v in rng.uniform(lo, hi, n)]
+    return {
+        "n_layers": n, "freeze_idx": int(freeze_idx), "train_batch": int(train_batch),
+        "request_images": int(request_images), "server_slots": int(server_slots),
+        "iterations": max(1, int(images_per_epoch) // int(train_batch)),
+        "image_bytes": [int(v) for v in image_bytes],
+        "srv_layer_s": layer(0.2e-3, 5e-3), "cli_layer_s": layer(0.5e-3, 20e-3),
+        "srv_read_data_s": float(rng.uniform(0.02, 0.08)),
+        "srv_read_model_s": float(rng.uniform(0.05, 0.3)),
+        "srv_to_gpu_s": float(rng.uniform(1e-3, 10e-3)),
+        "cli_rest_s": float(rng.uniform(0.05, 0.5)),
+        "srv_from_gpu_s_per_byte": 1.0 / float(rng.uniform(10e9, 25e9)),
+        "srv_pickle_s_per_byte": 1.0 / float(rng.uniform(1e9, 4e9)),
+        "cli_unpickle_s_per_byte": 1.0 / float(rng.uniform(1e9, 4e9)),
+        "cli_loader_s_per_byte": 1.0 / float(rng.uniform(2e9, 8e9)),
+        "cli_to_gpu_s_per_byte": 1.0 / float(rng.uniform(10e9, 25e9)),
+        "net_bytes_per_s": 1.5e9 * float(np.exp(rng.uniform(np.log(0.25), np.log(4.0)))),
+        "cli_mem_bytes": 0, "cli_fixed_mem_bytes": 0, "nosplit_iter_s": 0.0,
+    }

@@ -195,3 +195,28 @@ def test_fused_stem_pool_is_bit_exact(name):
     print(f"{name}: fused {tuple(fused.shape)} vs stem + pool {tuple(ref.shape)}", flush=True)
     assert fused.shape == ref.shape
     assert torch.equal(fused, ref)
+
+
+@pytest.mark.parametrize("name", ["resnet50", "vit_b16"])
+def test_split_choice_from_live_profile(name):
+    """The profile measured on the GPU (one 128-image request at a 16-image
+    storage-side batch) feeds Algorithm 1; the library's choice must equal the
+    oracle's on the same numbers."""
+    from oracle import split as OS
+    d = H.Desc(PM.FACTORIES[name](), H.HAPI_BF16, stream=torch.cuda.current_stream(), chunk=16)
+    need = H.hapi_workspace_bytes(d, 128, d.n_layers, True)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    d.set(workspace=ws, workspace_bytes=need)
+    _, us = H.hapi_profile_layers(d, 128, True)
+    per_image, _ = H.hapi_profile_layers(d, 1)
+    j = synth.split_job(90, per_image, d.n_layers - 1, train_batch=1024)
+    j["srv_layer_s"] = [0.0] + [t * 1e-6 for t in us[1:]]
+    choice, est = H.hapi_choose_split(**j)
+    split, runtimes, earliest = OS.choose_split(j)
+    print(f"{name}: server layer times {['%.0f' % t for t in us[1:]]} us; "
+          f"HAPI {choice['hapi']} (oracle {split}), NSG {choice['nsg']}, "
+          f"@Min {choice['min_output']}", flush=True)
+    assert choice["hapi"] == split and choice["earliest"] == earliest
+    assert choice["nsg"] == OS.nsg(j) and choice["min_output"] == OS.at_min(j)
+    for s, t in runtimes.items():
+        assert abs(est[s]["epoch_s"] - t) <= 1e-12 * t
