@@ -192,6 +192,21 @@ int32_t hapi_chunk_count(const hapi_model_desc *desc, int32_t batch);
 int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *images,
                  int32_t batch, int32_t split_layer, void *out);
 
+/* Resume from a split (the compute-tier half: System implementation, models
+ * that run the forward pass between arbitrary layers; Design, "Request flow",
+ * the client continues from the split layer's output).  Runs layers
+ * start_layer+1 .. end_layer on
+ *   input   [batch, <hapi_layer_shape(start_layer)>] in desc->dtype, the
+ *           caller layout hapi_extract writes (NCHW or [batch, T, D])
+ * and writes out as hapi_extract(end_layer) does.  0 <= start_layer <=
+ * end_layer <= n_layers; start_layer = 0 is hapi_extract, start_layer =
+ * end_layer copies the input.  The same kernels and rounding points run as in
+ * a single pass, so hapi_extract(s) followed by hapi_extract_range(s, e) gives
+ * hapi_extract(e) bit for bit.  Workspace: hapi_workspace_bytes(desc, batch,
+ * end_layer, 0).  Errors and stream semantics as hapi_extract. */
+int hapi_extract_range(const hapi_model_desc *desc, const void *weights, const void *input,
+                       int32_t batch, int32_t start_layer, int32_t end_layer, void *out);
+
 /* Per-layer profile for split selection (Table 1; Measurement study, Fig. 2a/2b).
  *   out_bytes[k], k = 0..n_layers: bytes of the layer-k output at `batch`
  *                 (k = 0: the input), closed form, no device access.

@@ -315,6 +315,19 @@ class Model:
                 outs.append(y)
         return outs if collect else y
 
+    def forward_range(self, params, x, start, end):
+        """Run layers start+1..end on x, the layer-``start`` activation in the
+        layout ``forward`` returns (System implementation: the forward pass
+        between arbitrary layers; the compute tier resumes from the split)."""
+        if not 0 <= start <= end <= self.n_layers:
+            raise ValueError(f"range {start}..{end} outside [0, {self.n_layers}]")
+        counts = self.param_counts()
+        p = iter(params[sum(counts[:start]):sum(counts[:end])])
+        y = np.asarray(x, np.float64)
+        for layer in self.layers[start:end]:
+            y = layer.forward(y, p)
+        return y
+
 
 def alexnet():
     """AlexNet feature layers: conv11/4(64)-pool-conv5(192)-pool-conv3(384)-conv3(256)-conv3(256)-pool."""

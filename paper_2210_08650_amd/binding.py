@@ -27,8 +27,8 @@ __all__ = ["HapiError", "Desc", "hapi_layer", "hapi_model_desc", "hapi_kernel_st
            "HAPI_VIT_BLOCK", "HAPI_LAYERNORM", "HAPI_DENSE_BLOCK", "LIB_PATH", "EXPORTED",
            "hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
            "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-           "hapi_profile_layers", "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error",
-           "hapi_split_job", "hapi_split_estimate", "hapi_split_choice", "hapi_choose_split"]
+           "hapi_extract_range", "hapi_profile_layers", "hapi_stats_enable",
+           "hapi_stats_collect", "hapi_last_error", "hapi_split_job", "hapi_split_estimate", "hapi_split_choice", "hapi_choose_split"]
 
 _STATUS = {HAPI_E_INVAL: "HAPI_E_INVAL", HAPI_E_UNSUPPORTED: "HAPI_E_UNSUPPORTED",
            HAPI_E_NOMEM: "HAPI_E_NOMEM", HAPI_E_DEVICE: "HAPI_E_DEVICE"}
@@ -124,6 +124,7 @@ def _load():
         "hapi_workspace_bytes": (i64, [D, i32, i32, i32]),
         "hapi_chunk_count": (i32, [D, i32]),
         "hapi_extract": (ctypes.c_int, [D, vp, vp, i32, i32, vp]),
+        "hapi_extract_range": (ctypes.c_int, [D, vp, vp, i32, i32, i32, vp]),
         "hapi_profile_layers": (ctypes.c_int, [D, i32, ctypes.POINTER(i64),
                                                ctypes.POINTER(ctypes.c_float)]),
         "hapi_stats_enable": (ctypes.c_int, [i32]),
@@ -142,8 +143,8 @@ def _load():
 _lib = _load()
 EXPORTED = ("hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
             "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-            "hapi_profile_layers", "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error",
-            "hapi_choose_split")
+            "hapi_extract_range", "hapi_profile_layers", "hapi_stats_enable",
+            "hapi_stats_collect", "hapi_last_error", "hapi_choose_split")
 
 
 def _ptr(p):
@@ -237,6 +238,12 @@ def hapi_chunk_count(desc: Desc, batch: int) -> int:
 def hapi_extract(desc: Desc, weights, images, batch: int, split_layer: int, out) -> None:
     _check(_lib.hapi_extract(desc.ref, _ptr(weights), _ptr(images), int(batch),
                              int(split_layer), _ptr(out)))
+
+
+def hapi_extract_range(desc: Desc, weights, input, batch: int, start_layer: int,
+                       end_layer: int, out) -> None:
+    _check(_lib.hapi_extract_range(desc.ref, _ptr(weights), _ptr(input), int(batch),
+                                   int(start_layer), int(end_layer), _ptr(out)))
 
 
 def hapi_profile_layers(desc: Desc, batch: int, time_layers: bool = False):

@@ -491,9 +491,20 @@ bool stem_pool_fusable(const Model &m) {
   return stem_pool_supported(l0.in.c, l0.in.h, l0.in.w, cs.cout, l0.out.h, l0.out.w, l1.out.h, l1.out.w);
 }
 
-// Runs layers 1..split on nb images; writes the split output (caller layout)
-// to `out` unless it is null (profiling).
-int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
+// The tensor in front of layer `start` + 1: the input (start = 0) or the
+// output of layer `start`.
+const Act &act_at(const Model &m, int start) {
+  return start == 0 ? m.input : m.layers[start - 1].out;
+}
+
+// A tensor whose caller layout equals the internal NHWC one: tokens, and
+// images of one pixel or one channel.
+bool layout_free(const Act &a) { return a.tok || a.h * a.w == 1 || a.c == 1; }
+
+// Runs layers start+1..split on nb images of `images` (the layer-`start`
+// tensor in the caller layout); writes the split output (caller layout) to
+// `out` unless it is null (profiling).
+int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, void *out) {
   const Model &m = c.m;
   const bool bf = m.bf16;
   const void *cur = images;
@@ -503,17 +514,26 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
       if (i != cur_slot && i != a && i != b) return i;
     return -1;
   };
-  if (!m.first_reads_nchw) {
-    HIP_TRY(timed(c.s, F_LAYOUT, 0.0, 2.0 * nb * m.input.elems() * m.esz, [&] {
-      return launch_nchw_to_nhwc(bf, images, c.slot[0], nb, m.input.h * m.input.w, m.input.c, c.s);
-    }));
+  // Stage the input in slot 0 in NHWC, except for a first layer that reads
+  // the caller's NCHW images itself.  Blocks update their input slot in
+  // place, so a resumed input is always staged, never used where it lies.
+  if (start > 0 || !m.first_reads_nchw) {
+    const Act &a = act_at(m, start);
+    const int64_t bytes = (int64_t)nb * a.elems() * m.esz;
+    if (layout_free(a)) {
+      HIP_TRY(timed(c.s, F_COPY, 0.0, 2.0 * bytes, [&] { return launch_copy(images, c.slot[0], bytes, c.s); }));
+    } else {
+      HIP_TRY(timed(c.s, F_LAYOUT, 0.0, 2.0 * bytes, [&] {
+        return launch_nchw_to_nhwc(bf, images, c.slot[0], nb, a.h * a.w, a.c, c.s);
+      }));
+    }
     cur = c.slot[0];
     cur_slot = 0;
   }
-  int li0 = 0;
+  int li0 = start;
   // Stem convolution and max pooling in one kernel when the stem output is
   // not itself the split and layers are not being timed one by one.
-  if (split >= 2 && !c.on_layer && stem_pool_fusable(m) && (uintptr_t)images % 4 == 0) {
+  if (start == 0 && split >= 2 && !c.on_layer && stem_pool_fusable(m) && (uintptr_t)images % 4 == 0) {
     const LayerPlan &l0 = m.layers[0], &l1 = m.layers[1];
     const ConvSpec &cs = l0.convs[0];
     const int o = free_slot();
@@ -712,7 +732,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
   if (out) {
     const Act &o = m.layers[split - 1].out;
     const int64_t bytes = (int64_t)nb * o.elems() * m.esz;
-    if (o.tok || o.h * o.w == 1 || o.c == 1) {
+    if (layout_free(o)) {
       HIP_TRY(timed(c.s, F_COPY, 0.0, 2.0 * bytes, [&] { return launch_copy(cur, out, bytes, c.s); }));
     } else {
       HIP_TRY(timed(c.s, F_LAYOUT, 0.0, 2.0 * bytes, [&] {
@@ -724,17 +744,17 @@ int run_chunk(const Ctx &c, const void *images, int nb, int split, void *out) {
 }
 
 int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, const void *images,
-              int batch, int split, void *out, uint8_t *ws, int chunk,
+              int batch, int start, int split, void *out, uint8_t *ws, int chunk,
               const std::function<void(int, bool)> &on_layer) {
   hipStream_t s = static_cast<hipStream_t>(d->stream);
   const int64_t sb = slot_bytes(m, split, chunk);
   Ctx c{m, s, static_cast<const uint8_t *>(weights), {ws, ws + sb, ws + 2 * sb}, on_layer};
-  const int64_t in_bytes = m.input.elems() * m.esz;
+  const int64_t in_bytes = act_at(m, start).elems() * m.esz;
   const int64_t out_bytes = m.layers[split - 1].out.elems() * m.esz;
   for (int b0 = 0; b0 < batch; b0 += chunk) {
     const int nb = std::min(chunk, batch - b0);
-    const int r = run_chunk(c, static_cast<const uint8_t *>(images) + (int64_t)b0 * in_bytes, nb, split,
-                            out ? static_cast<uint8_t *>(out) + (int64_t)b0 * out_bytes : nullptr);
+    const int r = run_chunk(c, static_cast<const uint8_t *>(images) + (int64_t)b0 * in_bytes, nb, start,
+                            split, out ? static_cast<uint8_t *>(out) + (int64_t)b0 * out_bytes : nullptr);
     if (r != HAPI_OK) return r;
   }
   return HAPI_OK;
@@ -836,8 +856,12 @@ int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void
   return HAPI_OK;
 }
 
-int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *images,
-                 int32_t batch, int32_t split_layer, void *out) {
+}  // extern "C"
+
+namespace {
+
+int extract_range(const hapi_model_desc *desc, const void *weights, const void *images,
+                  int32_t batch, int32_t start_layer, int32_t split_layer, void *out) {
   Model m;
   int r = analyze(desc, m);
   if (r != HAPI_OK) return r;
@@ -845,9 +869,11 @@ int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *i
   if (batch < 1) return fail(HAPI_E_INVAL, "batch must be >= 1");
   if (split_layer < 0 || split_layer > (int)m.layers.size())
     return fail(HAPI_E_INVAL, "split %d outside [0, %d]", split_layer, (int)m.layers.size());
+  if (start_layer < 0 || start_layer > split_layer)
+    return fail(HAPI_E_INVAL, "start layer %d outside [0, %d]", start_layer, split_layer);
   hipStream_t s = static_cast<hipStream_t>(desc->stream);
-  if (split_layer == 0) {  // no split: the raw input is the result
-    const int64_t bytes = (int64_t)batch * m.input.elems() * m.esz;
+  if (split_layer == start_layer) {  // nothing to run: the input is the result
+    const int64_t bytes = (int64_t)batch * act_at(m, start_layer).elems() * m.esz;
     HIP_TRY(timed(s, F_COPY, 0.0, 2.0 * bytes, [&] { return launch_copy(images, out, bytes, s); }));
     return HAPI_OK;
   }
@@ -863,8 +889,22 @@ int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *i
     return fail(HAPI_E_NOMEM, "workspace of %zu bytes, %lld needed", desc->workspace_bytes,
                 (long long)need);
   if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
-  return run_batch(desc, m, weights, images, batch, split_layer, out,
+  return run_batch(desc, m, weights, images, batch, start_layer, split_layer, out,
                    static_cast<uint8_t *>(desc->workspace), chunk, nullptr);
+}
+
+}  // namespace
+
+extern "C" {
+
+int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *images,
+                 int32_t batch, int32_t split_layer, void *out) {
+  return extract_range(desc, weights, images, batch, 0, split_layer, out);
+}
+
+int hapi_extract_range(const hapi_model_desc *desc, const void *weights, const void *input,
+                       int32_t batch, int32_t start_layer, int32_t end_layer, void *out) {
+  return extract_range(desc, weights, input, batch, start_layer, end_layer, out);
 }
 
 int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out_bytes,
@@ -923,7 +963,7 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
       (void)begin;
       (void)hipEventRecord(ev[idx++], s);
     };
-    rc = run_batch(desc, m, pk, img, batch, n, nullptr, ws, chunk, cb);
+    rc = run_batch(desc, m, pk, img, batch, 0, n, nullptr, ws, chunk, cb);
     if (rc != HAPI_OK) break;
     if (hipEventSynchronize(ev[idx - 1]) != hipSuccess) {
       rc = fail(HAPI_E_DEVICE, "hipEventSynchronize failed");

@@ -65,5 +65,17 @@ class Runner:
         torch.cuda.synchronize()
         return out
 
+    def resume(self, input_dev, start, end, chunk=0):
+        """Layers start+1..end on the layer-``start`` tensor (caller layout)."""
+        batch = input_dev.shape[0]
+        self.desc.set(chunk=chunk)
+        need = H.hapi_workspace_bytes(self.desc, batch, end)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device="cuda")
+        self.desc.set(workspace=ws, workspace_bytes=need)
+        out = torch.empty((batch,) + self.out_shape(end), dtype=self.tdtype, device="cuda")
+        H.hapi_extract_range(self.desc, self.packed, input_dev, batch, start, end, out)
+        torch.cuda.synchronize()
+        return out
+
     def extract_np(self, images_dev, split, chunk=0):
         return self.extract(images_dev, split, chunk).float().cpu().numpy()

@@ -220,3 +220,41 @@ def test_split_choice_from_live_profile(name):
     assert choice["nsg"] == OS.nsg(j) and choice["min_output"] == OS.at_min(j)
     for s, t in runtimes.items():
         assert abs(est[s]["epoch_s"] - t) <= 1e-12 * t
+
+
+RESUME_CASES = [("resnet18", ((1, 8), (2, 8), (4, 11), (8, 8), (0, 5))),
+                ("resnet50", ((1, 18), (2, 10), (10, 19))),
+                ("alexnet", ((2, 8), (5, 6))),
+                ("vgg16", ((3, 18), (9, 13))),
+                ("vit_b16", ((1, 6), (2, 10), (10, 15))),
+                ("densenet_block", ((1, 3), (2, 3)))]
+
+
+@pytest.mark.parametrize("name,pairs", RESUME_CASES)
+def test_resume_from_split_is_bit_exact(name, pairs):
+    """extract(0 -> s), then resume(s -> e), equals extract(0 -> e) bit for bit
+    (storage side and compute side run the same kernels and roundings)."""
+    r, _, _, xd, _, _ = _setup(name, 91, 3)
+    for s, e in pairs:
+        mid = r.extract(xd, s)
+        whole = r.extract(xd, e)
+        got = r.resume(mid, s, e)
+        print(f"{name}: resume {s} -> {e}, {tuple(got.shape)}", flush=True)
+        assert torch.equal(got, whole), (s, e)
+        if s < e:
+            assert torch.equal(r.resume(mid, s, e, chunk=2), whole), (s, e)
+
+
+@pytest.mark.parametrize("name,s,e", [("resnet50", 5, 12), ("alexnet", 3, 8),
+                                      ("vit_b16", 3, 6), ("densenet_block", 2, 3)])
+def test_resume_matches_oracle(name, s, e):
+    """The resumed layers on a synthetic layer-s tensor against the oracle."""
+    r, om, ps, _, _, dtype = _setup(name, 92, 2)
+    shp = om.shapes()[s]
+    x = synth.images(93, 2, 1, int(np.prod(shp[:-1])), shp[-1]).reshape((2,) + tuple(shp))
+    xd, xv = images_for(dtype, x)
+    got = r.resume(xd, s, e).float().cpu().numpy()
+    ref = om.forward_range(ps, xv, s, e)
+    err = rel_l2(got, ref)
+    print(f"{name}: resume {s} -> {e} rel_l2 {err:.3e}", flush=True)
+    assert got.shape == ref.shape and err <= TOL[dtype]

@@ -130,6 +130,17 @@ def test_validation_errors_before_any_launch():
     _raises(H.HAPI_E_NOMEM, H.hapi_extract, d, fake, fake, 4, 8, fake)
 
 
+def test_resume_validation_before_any_launch():
+    d = _desc("resnet18")
+    fake = 1 << 40
+    _raises(H.HAPI_E_INVAL, H.hapi_extract_range, d, fake, fake, 4, 5, 4, fake)
+    _raises(H.HAPI_E_INVAL, H.hapi_extract_range, d, fake, fake, 4, -1, 4, fake)
+    _raises(H.HAPI_E_INVAL, H.hapi_extract_range, d, fake, fake, 4, 2, 12, fake)
+    _raises(H.HAPI_E_INVAL, H.hapi_extract_range, d, fake, None, 4, 2, 8, fake)
+    _raises(H.HAPI_E_NOMEM, H.hapi_extract_range, d.set(workspace=fake, workspace_bytes=1),
+            fake, fake, 4, 2, 8, fake)
+
+
 def test_unsupported_and_invalid_descriptors():
     bad_head = PM.vit(dim=768, heads=8)          # head dim 96 is not built
     _raises(H.HAPI_E_UNSUPPORTED, H.hapi_raw_weight_count, H.Desc(bad_head, H.HAPI_BF16))

@@ -396,6 +396,22 @@ def test_split_zero_is_input():
     assert np.array_equal(m.forward(synth.params(0, m.manifest()), x, 0), x.astype(np.float64))
 
 
+@pytest.mark.parametrize("name", ["resnet18", "vit_small"])
+def test_forward_range_composes_to_forward(name):
+    # Resuming from any split reproduces the single pass exactly (same float64
+    # operations in the same order); a wrong parameter offset breaks it.
+    m = M.resnet18(in_hw=64) if name == "resnet18" else \
+        M.vit(image=64, patch=16, dim=128, heads=2, mlp=256, depth=2, name="vit_small")
+    ps = synth.params(56, m.manifest())
+    x = synth.images(56, 2, height=64, width=64)
+    outs = m.forward(ps, x, m.n_layers, collect=True)
+    for s in range(m.n_layers + 1):
+        for e in range(s, m.n_layers + 1):
+            assert np.array_equal(m.forward_range(ps, outs[s], s, e), outs[e]), (s, e)
+    with pytest.raises(ValueError):
+        m.forward_range(ps, x, 2, 1)
+
+
 # ----------------------------------------------------------- dense block
 
 def _torch_dense_block(x, params, n, growth):
