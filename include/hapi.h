@@ -87,6 +87,10 @@ typedef enum { HAPI_F32 = 0, HAPI_BF16 = 1 } hapi_dtype;
  *                  layer l maps the c = cin + l * growth channels so far to
  *                  conv3x3(ReLU(BN2(conv1x1(ReLU(BN1(x)))))) (growth channels,
  *                  pad 1) and concatenates them after the existing channels.
+ * HAPI_PREACT_CONV cin, cout, k, stride, pad: pre-activation convolution
+ *                  y = W * ReLU(BN(x)), no bias (DenseNet transition; the
+ *                  batch-norm acts on the input, so it cannot fold into W).
+ * HAPI_BATCHNORM   cout (= channels), relu: y = [ReLU](BN(x)) per channel.
  *
  * Batch-norm is inference-mode with eps 1e-5. */
 typedef enum {
@@ -99,7 +103,9 @@ typedef enum {
   HAPI_TOKENS = 6,
   HAPI_VIT_BLOCK = 7,
   HAPI_LAYERNORM = 8,
-  HAPI_DENSE_BLOCK = 9
+  HAPI_DENSE_BLOCK = 9,
+  HAPI_PREACT_CONV = 10,
+  HAPI_BATCHNORM = 11
 } hapi_kind;
 
 typedef struct {
@@ -141,6 +147,8 @@ typedef struct {
  *   DENSE_BLOCK  per dense layer l (c = cin + l * growth): bn1 gamma, beta, mean,
  *                var [c]; conv1 weight [bottleneck, c, 1, 1]; bn2 gamma, beta,
  *                mean, var [bottleneck]; conv2 weight [growth, bottleneck, 3, 3]
+ *   PREACT_CONV  bn gamma, beta, mean, var [cin]; weight [cout, cin, k, k]
+ *   BATCHNORM    gamma, beta, mean, var [cout]
  * Returns the number of float32 values, or a negative hapi_status. */
 int64_t hapi_raw_weight_count(const hapi_model_desc *desc);
 

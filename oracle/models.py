@@ -91,6 +91,65 @@ class MaxPool:
         return L.maxpool2d(x, self.k, self.stride, self.pad)
 
 
+class AvgPool:
+    """k x k window mean with stride, no padding (DenseNet transition pooling)."""
+
+    def __init__(self, k, stride):
+        self.k, self.stride = k, stride
+
+    def manifest(self):
+        return []
+
+    def out_shape(self, s):
+        c, h, w = s
+        return (c, (h - self.k) // self.stride + 1, (w - self.k) // self.stride + 1)
+
+    def forward(self, x, p):
+        return L.avgpool2d(x, self.k, self.stride)
+
+
+class PreActConv:
+    """Pre-activation convolution y = conv(ReLU(BN(x))), no bias: the DenseNet
+    transition's batch-norm and ReLU act on its input."""
+
+    def __init__(self, cin, cout, k=1, stride=1, pad=0):
+        self.cin, self.cout, self.k, self.stride, self.pad = cin, cout, k, stride, pad
+
+    def manifest(self):
+        return _bn_manifest(self.cin) + [((self.cout, self.cin, self.k, self.k), "he")]
+
+    def out_shape(self, s):
+        c, h, w = s
+        assert c == self.cin
+        return (self.cout, (h + 2 * self.pad - self.k) // self.stride + 1,
+                (w + 2 * self.pad - self.k) // self.stride + 1)
+
+    def forward(self, x, p):
+        g, b, m, v = next(p), next(p), next(p), next(p)
+        w = next(p)
+        h = L.relu(L.batchnorm(x, g, b, m, v, BN_EPS))
+        return L.conv2d(h, w, None, self.stride, self.pad)
+
+
+class BatchNorm:
+    """Inference batch-norm over channels, optionally followed by ReLU."""
+
+    def __init__(self, c, relu=False):
+        self.c, self.relu = c, relu
+
+    def manifest(self):
+        return _bn_manifest(self.c)
+
+    def out_shape(self, s):
+        assert s[0] == self.c
+        return s
+
+    def forward(self, x, p):
+        g, b, m, v = next(p), next(p), next(p), next(p)
+        y = L.batchnorm(x, g, b, m, v, BN_EPS)
+        return L.relu(y) if self.relu else y
+
+
 class GlobalAvgPool:
     def manifest(self):
         return []
@@ -383,6 +442,23 @@ def dense_block_net(in_hw=224, n_layers=4, growth=32, bottleneck=128):
                                     DenseBlock(64, n_layers, growth, bottleneck)], (3, in_hw, in_hw))
 
 
+def densenet121(in_hw=224, growth=32, bottleneck=128, blocks=(6, 12, 24, 16)):
+    """DenseNet-121 features (TorchVision layout): conv 7x7/2 + BN + ReLU,
+    maxpool 3x3/2, four dense blocks; between blocks a transition of BN, ReLU,
+    1x1 convolution halving the channels and 2x2/2 average pooling (here two
+    layers: the pre-activation convolution and the pooling); a closing BN."""
+    layers = [Conv(3, 64, 7, 2, 3, bn=True), MaxPool(3, 2, 1)]
+    c = 64
+    for i, n in enumerate(blocks):
+        layers.append(DenseBlock(c, n, growth, bottleneck))
+        c += n * growth
+        if i + 1 < len(blocks):
+            layers += [PreActConv(c, c // 2), AvgPool(2, 2)]
+            c //= 2
+    layers.append(BatchNorm(c))
+    return Model("densenet121", layers, (3, in_hw, in_hw))
+
+
 def vit(image=224, patch=16, dim=768, heads=12, mlp=3072, depth=12, name="vit_b16"):
     """Vision Transformer encoder: patch embed, tokens, ``depth`` blocks, final LN."""
     g = image // patch
@@ -406,7 +482,8 @@ WORKLOADS = {
 }
 
 FACTORIES = {"alexnet": alexnet, "resnet18": resnet18, "resnet50": resnet50,
-             "vgg16": vgg16, "vit_b16": vit_b16, "densenet_block": dense_block_net}
+             "vgg16": vgg16, "vit_b16": vit_b16, "densenet_block": dense_block_net,
+             "densenet121": densenet121}
 
 
 def build(name):

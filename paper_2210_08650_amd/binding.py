@@ -18,13 +18,15 @@ LIB_PATH = os.path.join(_HERE, "libhapi.so")
 HAPI_OK, HAPI_E_INVAL, HAPI_E_UNSUPPORTED, HAPI_E_NOMEM, HAPI_E_DEVICE = 0, -1, -2, -3, -4
 HAPI_F32, HAPI_BF16 = 0, 1
 (HAPI_CONV, HAPI_MAXPOOL, HAPI_AVGPOOL, HAPI_BASIC_BLOCK, HAPI_BOTTLENECK, HAPI_PATCH_EMBED,
- HAPI_TOKENS, HAPI_VIT_BLOCK, HAPI_LAYERNORM, HAPI_DENSE_BLOCK) = range(10)
+ HAPI_TOKENS, HAPI_VIT_BLOCK, HAPI_LAYERNORM, HAPI_DENSE_BLOCK, HAPI_PREACT_CONV,
+ HAPI_BATCHNORM) = range(12)
 
 __all__ = ["HapiError", "Desc", "hapi_layer", "hapi_model_desc", "hapi_kernel_stat",
            "HAPI_OK", "HAPI_E_INVAL", "HAPI_E_UNSUPPORTED", "HAPI_E_NOMEM", "HAPI_E_DEVICE",
            "HAPI_F32", "HAPI_BF16", "HAPI_CONV", "HAPI_MAXPOOL", "HAPI_AVGPOOL",
            "HAPI_BASIC_BLOCK", "HAPI_BOTTLENECK", "HAPI_PATCH_EMBED", "HAPI_TOKENS",
-           "HAPI_VIT_BLOCK", "HAPI_LAYERNORM", "HAPI_DENSE_BLOCK", "LIB_PATH", "EXPORTED",
+           "HAPI_VIT_BLOCK", "HAPI_LAYERNORM", "HAPI_DENSE_BLOCK", "HAPI_PREACT_CONV",
+           "HAPI_BATCHNORM", "LIB_PATH", "EXPORTED",
            "hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
            "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
            "hapi_extract_range", "hapi_profile_layers", "hapi_stats_enable",

@@ -292,6 +292,30 @@ int analyze(const hapi_model_desc *d, Model &m) {
         lp.out = cur;
         break;
       }
+      case HAPI_PREACT_CONV: {
+        if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: PREACT_CONV needs bf16", li + 1);
+        if (cur.tok || L.cin != cur.c)
+          return fail(HAPI_E_INVAL, "layer %d: PREACT_CONV input mismatch", li + 1);
+        if (L.k < 1 || L.stride < 1 || L.pad < 0 || L.cout < 1)
+          return fail(HAPI_E_INVAL, "layer %d: bad conv geometry", li + 1);
+        if (first || !nhwc_ok(L.cin))
+          return fail(HAPI_E_UNSUPPORTED, "layer %d: PREACT_CONV needs cin %% %d == 0 after the first layer",
+                      li + 1, kq);
+        const int ho = conv_out(cur.h, L.k, L.stride, L.pad), wo = conv_out(cur.w, L.k, L.stride, L.pad);
+        if (ho < 1 || wo < 1) return fail(HAPI_E_INVAL, "layer %d: empty conv output", li + 1);
+        add_bn_affine(lp, L.cin);
+        add_conv(lp, L.cin, L.cout, L.k, L.stride, L.pad, false, false);
+        lp.out = Act{L.cout, ho, wo, false};
+        break;
+      }
+      case HAPI_BATCHNORM: {
+        if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: BATCHNORM needs bf16", li + 1);
+        if (cur.tok || L.cout != cur.c) return fail(HAPI_E_INVAL, "layer %d: BATCHNORM input mismatch", li + 1);
+        if (L.cout % 8 != 0) return fail(HAPI_E_UNSUPPORTED, "layer %d: BATCHNORM needs channels %% 8 == 0", li + 1);
+        add_bn_affine(lp, L.cout);
+        lp.out = cur;
+        break;
+      }
       case HAPI_DENSE_BLOCK: {
         if (!m.bf16) return fail(HAPI_E_UNSUPPORTED, "layer %d: DENSE_BLOCK needs bf16", li + 1);
         if (cur.tok || L.cin != cur.c) return fail(HAPI_E_INVAL, "layer %d: DENSE_BLOCK input mismatch", li + 1);
@@ -694,6 +718,35 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         cur_slot = o;
         break;
       }
+      case HAPI_PREACT_CONV: {
+        // Batch-norm + ReLU in front of the convolution cannot fold into its
+        // weights; it runs on the input, then the plain convolution.
+        const int A = free_slot(), B = free_slot(A);
+        const int64_t pixels = (int64_t)nb * lp.in.h * lp.in.w;
+        const Extra &bn = lp.extras[0];
+        HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * lp.in.c, 2.0 * pixels * lp.in.c * m.esz, [&] {
+          return launch_affine(cur, reinterpret_cast<const float *>(c.pk + bn.pk),
+                               reinterpret_cast<const float *>(c.pk + bn.pk) + bn.n, c.slot[A], pixels,
+                               lp.in.c, lp.in.c, true, c.s);
+        }));
+        HIP_TRY(run_conv(c, lp.convs[0], c.slot[A], lp.in, nb, c.slot[B], nullptr, false, false, false));
+        cur = c.slot[B];
+        cur_slot = B;
+        break;
+      }
+      case HAPI_BATCHNORM: {
+        const int o = free_slot();
+        const int64_t pixels = (int64_t)nb * lp.in.h * lp.in.w;
+        const Extra &bn = lp.extras[0];
+        HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * lp.in.c, 2.0 * pixels * lp.in.c * m.esz, [&] {
+          return launch_affine(cur, reinterpret_cast<const float *>(c.pk + bn.pk),
+                               reinterpret_cast<const float *>(c.pk + bn.pk) + bn.n, c.slot[o], pixels,
+                               lp.in.c, lp.in.c, L.relu != 0, c.s);
+        }));
+        cur = c.slot[o];
+        cur_slot = o;
+        break;
+      }
       case HAPI_DENSE_BLOCK: {
         // Concatenation without copies: the block input is copied once into the
         // first channels of a buffer with all cout channels, and each dense
@@ -710,9 +763,9 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
           const int ch = lp.in.c + (int)l * growth;
           const Extra &bn = lp.extras[l];
           HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * ch, 2.0 * pixels * ch * m.esz, [&] {
-            return launch_affine_relu(cat, reinterpret_cast<const float *>(c.pk + bn.pk),
-                                      reinterpret_cast<const float *>(c.pk + bn.pk) + bn.n, c.slot[H],
-                                      pixels, ch, cout, c.s);
+            return launch_affine(cat, reinterpret_cast<const float *>(c.pk + bn.pk),
+                                 reinterpret_cast<const float *>(c.pk + bn.pk) + bn.n, c.slot[H], pixels,
+                                 ch, cout, true, c.s);
           }));
           const Act hin{ch, lp.in.h, lp.in.w, false};
           const Act tin{bott, lp.in.h, lp.in.w, false};

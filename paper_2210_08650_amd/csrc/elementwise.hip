@@ -342,10 +342,12 @@ __global__ void channel_copy_kernel(const uint16_t *__restrict__ x, uint16_t *__
       *reinterpret_cast<const uint4 *>(x + p * cx + g * 8);
 }
 
-// Pre-activation batch-norm + ReLU on a channel prefix, 8 channels per thread.
-__global__ void affine_relu_kernel(const uint16_t *__restrict__ x, const float *__restrict__ scale,
-                                   const float *__restrict__ shift, uint16_t *__restrict__ y,
-                                   int64_t pixels, int C, int cx) {
+// Inference batch-norm (per-channel scale and shift) and optional ReLU on a
+// channel prefix of C of the cx channels of x, 8 channels per thread.
+template <bool RELU>
+__global__ void affine_kernel(const uint16_t *__restrict__ x, const float *__restrict__ scale,
+                              const float *__restrict__ shift, uint16_t *__restrict__ y,
+                              int64_t pixels, int C, int cx) {
   const int cg = C / 8;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= pixels * cg) return;
@@ -357,8 +359,12 @@ __global__ void affine_relu_kernel(const uint16_t *__restrict__ x, const float *
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int c = g * 8 + 2 * j;
-    const float lo = fmaxf(bf2f((uint16_t)(w4[j] & 0xffff)) * scale[c] + shift[c], 0.0f);
-    const float hi = fmaxf(bf2f((uint16_t)(w4[j] >> 16)) * scale[c + 1] + shift[c + 1], 0.0f);
+    float lo = bf2f((uint16_t)(w4[j] & 0xffff)) * scale[c] + shift[c];
+    float hi = bf2f((uint16_t)(w4[j] >> 16)) * scale[c + 1] + shift[c + 1];
+    if (RELU) {
+      lo = fmaxf(lo, 0.0f);
+      hi = fmaxf(hi, 0.0f);
+    }
     o[j] = f2bf2(lo, hi);
   }
   *reinterpret_cast<uint4 *>(y + p * C + g * 8) = make_uint4(o[0], o[1], o[2], o[3]);
@@ -383,11 +389,11 @@ hipError_t launch_channel_copy(const void *x, void *y, int64_t pixels, int C, in
   return hipGetLastError();
 }
 
-hipError_t launch_affine_relu(const void *x, const float *scale, const float *shift, void *y,
-                              int64_t pixels, int C, int cx, hipStream_t s) {
+hipError_t launch_affine(const void *x, const float *scale, const float *shift, void *y,
+                         int64_t pixels, int C, int cx, bool relu, hipStream_t s) {
   const int64_t total = pixels * (C / 8);
-  hapi_launch(affine_relu_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                     (const uint16_t *)x, scale, shift, (uint16_t *)y, pixels, C, cx);
+  hapi_launch(relu ? affine_kernel<true> : affine_kernel<false>, dim3(blocks_for(total, 256)),
+              dim3(256), 0, s, (const uint16_t *)x, scale, shift, (uint16_t *)y, pixels, C, cx);
   return hipGetLastError();
 }
 

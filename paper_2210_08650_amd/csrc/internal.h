@@ -140,10 +140,11 @@ hipError_t launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s);
 // for `pixels` NHWC pixels.  C, cx, cy, off multiples of 8.  bf16.
 hipError_t launch_channel_copy(const void *x, void *y, int64_t pixels, int C, int cx, int cy,
                                int off, hipStream_t s);
-// Per-channel affine + ReLU over the first C channels of NHWC pixels with row
-// stride cx: y[p * C + c] = max(0, x[p * cx + c] * scale[c] + shift[c]).  bf16.
-hipError_t launch_affine_relu(const void *x, const float *scale, const float *shift, void *y,
-                              int64_t pixels, int C, int cx, hipStream_t s);
+// Per-channel affine (+ ReLU) over the first C channels of NHWC pixels with
+// row stride cx: y[p * C + c] = [max(0,] x[p * cx + c] * scale[c] + shift[c]).
+// C and cx multiples of 8.  bf16.
+hipError_t launch_affine(const void *x, const float *scale, const float *shift, void *y,
+                         int64_t pixels, int C, int cx, bool relu, hipStream_t s);
 // Inference batch-norm as a per-channel affine: scale = g / sqrt(v + 1e-5),
 // shift = b - m * scale, from raw [g | b | m | v] (C each).
 hipError_t launch_pack_affine(const float *bn, int C, float *scale, float *shift, hipStream_t s);

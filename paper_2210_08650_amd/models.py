@@ -9,9 +9,9 @@ distribution each synthetic stand-in for pre-trained weights is drawn from.
 """
 from __future__ import annotations
 
-from .binding import (HAPI_AVGPOOL, HAPI_BASIC_BLOCK, HAPI_BF16, HAPI_BOTTLENECK, HAPI_CONV,
-                      HAPI_DENSE_BLOCK, HAPI_F32, HAPI_LAYERNORM, HAPI_MAXPOOL, HAPI_PATCH_EMBED,
-                      HAPI_TOKENS, HAPI_VIT_BLOCK)
+from .binding import (HAPI_AVGPOOL, HAPI_BASIC_BLOCK, HAPI_BATCHNORM, HAPI_BF16, HAPI_BOTTLENECK,
+                      HAPI_CONV, HAPI_DENSE_BLOCK, HAPI_F32, HAPI_LAYERNORM, HAPI_MAXPOOL,
+                      HAPI_PATCH_EMBED, HAPI_PREACT_CONV, HAPI_TOKENS, HAPI_VIT_BLOCK)
 
 
 def conv(cin, cout, k, stride=1, pad=0, bias=False, bn=False, relu=True):
@@ -82,6 +82,31 @@ def dense_block_net(n_layers=4, growth=32, bottleneck=128):
             dense_block(64, n_layers, growth, bottleneck)]
 
 
+def preact_conv(cin, cout, k=1, stride=1, pad=0):
+    return dict(kind=HAPI_PREACT_CONV, cin=cin, cout=cout, k=k, stride=stride, pad=pad)
+
+
+def batchnorm(c, relu=False):
+    return dict(kind=HAPI_BATCHNORM, cout=c, relu=int(relu))
+
+
+def densenet121(growth=32, bottleneck=128, blocks=(6, 12, 24, 16)):
+    """DenseNet-121 features: stem and pooling, four dense blocks with a
+    transition (pre-activation 1x1 convolution halving the channels, then 2x2
+    average pooling) between them, and the closing batch-norm.  13 layers;
+    the paper's freeze layer (after the fourth dense block) is layer 12."""
+    layers = [conv(3, 64, 7, 2, 3, bn=True), maxpool(3, 2, 1)]
+    c = 64
+    for i, n in enumerate(blocks):
+        layers.append(dense_block(c, n, growth, bottleneck))
+        c += n * growth
+        if i + 1 < len(blocks):
+            layers += [preact_conv(c, c // 2), avgpool(2, 2)]
+            c //= 2
+    layers.append(batchnorm(c))
+    return layers
+
+
 def vit(image=224, patch=16, dim=768, heads=12, mlp=3072, depth=12):
     layers = [dict(kind=HAPI_PATCH_EMBED, cin=3, cout=dim, k=patch, stride=patch),
               dict(kind=HAPI_TOKENS, cout=dim)]
@@ -96,7 +121,8 @@ def vit_b16():
 
 
 FACTORIES = {"alexnet": alexnet, "resnet18": resnet18, "resnet50": resnet50,
-             "vgg16": vgg16, "vit_b16": vit_b16, "densenet_block": dense_block_net}
+             "vgg16": vgg16, "vit_b16": vit_b16, "densenet_block": dense_block_net,
+             "densenet121": densenet121}
 
 # The five benchmark workloads.  ``seed`` selects the synthetic input stream.
 WORKLOADS = {
@@ -108,6 +134,9 @@ WORKLOADS = {
     # synthetic 4-layer dense block (growth 32, 56 x 56) for the channel-concat path
     "densenet_block_bf16_b64": dict(seed=5, model="densenet_block", dtype=HAPI_BF16, batch=64,
                                     split=3),
+    # DenseNet-121 to its freeze layer (after the fourth dense block)
+    "densenet121_bf16_b256": dict(seed=6, model="densenet121", dtype=HAPI_BF16, batch=256,
+                                  split=12),
 }
 
 
@@ -164,6 +193,12 @@ def raw_manifest(layers, in_shape=(3, 224, 224)):
                   ((F, D), "tn02"), ((F,), "tn02"), ((D, F), "tn02"), ((D,), "tn02")]
         elif kind == HAPI_LAYERNORM:
             m += [((L["cout"],), "ln_gamma"), ((L["cout"],), "ln_beta")]
+        elif kind == HAPI_PREACT_CONV:
+            m += _bn(L["cin"]) + [((L["cout"], L["cin"], L["k"], L["k"]), "he")]
+            k, s, p = L["k"], L.get("stride", 1), L.get("pad", 0)
+            c, h, w = L["cout"], (h + 2 * p - k) // s + 1, (w + 2 * p - k) // s + 1
+        elif kind == HAPI_BATCHNORM:
+            m += _bn(L["cout"])
         elif kind == HAPI_DENSE_BLOCK:
             g, bt = L["width"], L["mlp_dim"]
             for ch in range(L["cin"], L["cout"], g):

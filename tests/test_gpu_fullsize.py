@@ -18,7 +18,8 @@ pytestmark = pytest.mark.gpu
 
 SAMPLES = {"alexnet_f32_b4": [0, 1, 2, 3], "resnet18_bf16_b64": [0, 17, 63],
            "vgg16_bf16_b128": [0, 127], "resnet50_bf16_b256": [0, 97, 255],
-           "vit_b16_bf16_b128": [0, 64, 127], "densenet_block_bf16_b64": [0, 31, 63]}
+           "vit_b16_bf16_b128": [0, 64, 127], "densenet_block_bf16_b64": [0, 31, 63],
+           "densenet121_bf16_b256": [0, 255]}
 
 
 @pytest.mark.parametrize("wl", list(PM.WORKLOADS))

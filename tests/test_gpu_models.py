@@ -32,7 +32,8 @@ def _setup(name, seed, batch, layers=None, omodel=None, in_shape=(3, 224, 224), 
 
 
 @pytest.mark.parametrize("name,batch", [("alexnet", 4), ("resnet18", 3), ("resnet50", 2),
-                                        ("vgg16", 2), ("vit_b16", 2), ("densenet_block", 3)])
+                                        ("vgg16", 2), ("vit_b16", 2), ("densenet_block", 3),
+                                        ("densenet121", 2)])
 def test_every_split_matches_oracle(name, batch):
     r, om, ps, xd, xv, dtype = _setup(name, 10 + len(name), batch)
     outs = om.forward(ps, xv, om.n_layers, collect=True)
@@ -47,6 +48,7 @@ def test_every_split_matches_oracle(name, batch):
 
 
 @pytest.mark.parametrize("name,split,chunks", [("resnet18", 8, (1, 2, 5)),
+                                                ("densenet121", 12, (2,)),
                                                 ("alexnet", 8, (1, 3)),
                                                 ("vit_b16", 4, (1, 3))])
 def test_chunking_is_bit_exact(name, split, chunks):
@@ -182,7 +184,7 @@ def test_kernel_stats_count_launches():
     assert st["conv_bf16"]["launches"] == 1 + 3 and "maxpool" not in st
 
 
-@pytest.mark.parametrize("name", ["resnet18", "resnet50", "densenet_block"])
+@pytest.mark.parametrize("name", ["resnet18", "resnet50", "densenet_block", "densenet121"])
 def test_fused_stem_pool_is_bit_exact(name):
     """With the split past the max pooling, the stem convolution and the
     pooling run as one kernel; its output must equal, bit for bit, the stem
@@ -227,7 +229,8 @@ RESUME_CASES = [("resnet18", ((1, 8), (2, 8), (4, 11), (8, 8), (0, 5))),
                 ("alexnet", ((2, 8), (5, 6))),
                 ("vgg16", ((3, 18), (9, 13))),
                 ("vit_b16", ((1, 6), (2, 10), (10, 15))),
-                ("densenet_block", ((1, 3), (2, 3)))]
+                ("densenet_block", ((1, 3), (2, 3))),
+                ("densenet121", ((2, 12), (4, 9), (5, 13)))]
 
 
 @pytest.mark.parametrize("name,pairs", RESUME_CASES)

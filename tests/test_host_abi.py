@@ -15,7 +15,7 @@ from paper_2210_08650_amd import models as PM
 from oracle import models as OM
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-NAMES = ["alexnet", "resnet18", "resnet50", "vgg16", "vit_b16", "densenet_block"]
+NAMES = ["alexnet", "resnet18", "resnet50", "vgg16", "vit_b16", "densenet_block", "densenet121"]
 
 
 def _desc(name, **kw):

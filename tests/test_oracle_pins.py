@@ -375,6 +375,14 @@ def test_paper_facts():
         e = M.build(name).out_elems()
         for k in ours:
             assert e[k] < e[k + 1] and e[k] < e[k - 1]
+    # DenseNet: stem conv, bn, relu and pool; four dense blocks; three
+    # transitions of bn, relu, conv and pool; the closing bn; the classifier.
+    # Ours: stem (bn, relu fused), pool, blocks, 2 layers per transition,
+    # the closing bn; the paper's freeze layer 20 ends the fourth block.
+    dn = M.densenet121()
+    assert dn.n_layers + 2 + 3 * 2 + 1 == t2["DenseNet"]["total"]
+    blocks = [i + 1 for i, layer in enumerate(dn.layers) if isinstance(layer, M.DenseBlock)]
+    assert blocks[-1] + 2 + 3 * 2 == t2["DenseNet"]["freeze"]
     # @Min over layers 1..freeze of the Transformer is layer 1 (earliest on ties).
     e = M.vit_b16().out_elems()
     assert e[1] == e[0]                      # patch embedding output = input size
@@ -445,6 +453,46 @@ def test_dense_block_with_zero_growth_convs_appends_zeros():
     x = np.random.default_rng(16).standard_normal((1, 8, 5, 5))
     y = blk.forward(x, iter(ps))
     assert np.array_equal(y[:, :8], x) and not y[:, 8:].any()
+
+
+def _torch_densenet121(x, params, blocks=(6, 12, 24, 16), growth=32):
+    """DenseNet-121 features restated with torch.nn.functional (float64),
+    returning every layer boundary the oracle exposes."""
+    it = iter(params)
+    nxt = lambda: _t(next(it))
+    bn = lambda v, g, b, m, var: F.batch_norm(v, m, var, g, b, training=False, eps=1e-5)
+    outs = [_t(x)]
+    w = nxt(); g, b, m, v = nxt(), nxt(), nxt(), nxt()
+    y = F.relu(bn(F.conv2d(outs[0], w, stride=2, padding=3), g, b, m, v))
+    outs.append(y)
+    outs.append(F.max_pool2d(y, 3, 2, 1))
+    c = 64
+    for i, n in enumerate(blocks):
+        blk = list(next(it) for _ in range(10 * n))
+        outs.append(_t(_torch_dense_block(outs[-1].numpy(), blk, n, growth)))
+        c += n * growth
+        if i + 1 < len(blocks):
+            g, b, m, v = nxt(), nxt(), nxt(), nxt()
+            w = nxt()
+            outs.append(F.conv2d(F.relu(bn(outs[-1], g, b, m, v)), w))
+            outs.append(F.avg_pool2d(outs[-1], 2, 2))
+            c //= 2
+    g, b, m, v = nxt(), nxt(), nxt(), nxt()
+    outs.append(bn(outs[-1], g, b, m, v))
+    return [o.numpy() for o in outs]
+
+
+def test_densenet121_vs_torch_functional():
+    m = M.densenet121(in_hw=64)
+    ps = synth.params(57, m.manifest())
+    x = synth.images(57, 2, height=64, width=64)
+    ours = m.forward(ps, x, m.n_layers, collect=True)
+    ref = _torch_densenet121(x, ps)
+    assert len(ours) == len(ref) == 14
+    for k, (a, r) in enumerate(zip(ours, ref)):
+        assert a.shape == r.shape, k
+        np.testing.assert_allclose(a, r, rtol=1e-9, atol=1e-9 * np.abs(r).max(), err_msg=str(k))
+    assert ours[12].shape == (2, 1024, 2, 2)
 
 
 def test_dense_block_net_shapes():

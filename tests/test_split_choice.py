@@ -20,7 +20,7 @@ import synth
 from oracle import models as OM
 from oracle import split as OS
 
-NAMES = ["alexnet", "resnet18", "resnet50", "vgg16", "vit_b16", "densenet_block"]
+NAMES = ["alexnet", "resnet18", "resnet50", "vgg16", "vit_b16", "densenet_block", "densenet121"]
 
 
 def _image_bytes(name):
