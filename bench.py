@@ -4,13 +4,15 @@ Default workload: ResNet-50 (Bottleneck [3, 4, 6, 3]), inference batch-norm
 folded, bf16 weights and activations with fp32 accumulation, batch 256 of
 synthetic 3x224x224 images, split after layer4 (2048x7x7, layer 18).  One step
 is one ``hapi_extract`` call over the whole batch: every layer from the input
-to the split, plus writing the split activations in NCHW.  Weights are packed
-once beforehand (model reuse); images and weights are resident in HBM.
+to the split, plus writing the split activations in NCHW; by default the
+library runs it as two 128-image partitions in flight on two streams.
+Weights are packed once beforehand (model reuse); images and weights are
+resident in HBM.
 
-Prints ONE JSON line with the throughput, the MFMA utilisation of the
-convolution kernels, a roofline entry for the dominant kernel family (timed
-with HIP events on the library's stream) and the CPU oracle timed on a bounded
-sample as a baseline.
+Prints ONE JSON line with the throughput, the share of the step's MFMA
+capacity the convolutions used, a roofline entry for the dominant kernel
+family (HIP events recorded by each launch on the stream it runs on) and the
+CPU oracle timed on a bounded sample as a baseline.
 """
 from __future__ import annotations
 
@@ -79,6 +81,70 @@ def cpu_baseline(cfg, budget_s=15.0):
                       f"{dt:.1f} s"}
 
 
+def concurrent_requests(args):
+    """The storage server's request pattern: each step serves ``requests``
+    requests of ``request_images`` images (one training iteration), split into
+    storage-side partitions of ``chunk`` images (default 16), with
+    ``concurrency`` requests in flight at once, each on its own stream and
+    workspace, issued by its own host thread."""
+    import threading
+    import torch
+    import paper_2210_08650_amd as H
+    from paper_2210_08650_amd import models as PM
+    import synth
+
+    cfg = dict(PM.WORKLOADS[args.workload])
+    S, R, Q = args.concurrency, args.requests, args.request_images
+    chunk = args.chunk or 16
+    layers = PM.FACTORIES[cfg["model"]]()
+    tdt = torch.bfloat16 if cfg["dtype"] == H.HAPI_BF16 else torch.float32
+    split = cfg["split"]
+    streams = [torch.cuda.Stream() for _ in range(S)]
+    descs, spaces = [], []
+    for t in range(S):
+        d = H.Desc(layers, cfg["dtype"], stream=streams[t], chunk=chunk)
+        need = H.hapi_workspace_bytes(d, Q, split)
+        spaces.append(torch.empty(max(need, 256), dtype=torch.uint8, device="cuda"))
+        descs.append(d.set(workspace=spaces[t], workspace_bytes=need))
+    raw = torch.from_numpy(synth.flatten(synth.params(cfg["seed"], PM.raw_manifest(layers)))).cuda()
+    packed = torch.empty(H.hapi_packed_weight_bytes(descs[0]), dtype=torch.uint8, device="cuda")
+    H.hapi_pack_weights(H.Desc(layers, cfg["dtype"]), raw, packed)
+    images = torch.from_numpy(synth.images(cfg["seed"], R * Q)).to(tdt).cuda()
+    out = torch.empty((R, Q) + H.hapi_layer_shape(descs[0], split), dtype=tdt, device="cuda")
+    torch.cuda.synchronize()
+    del raw
+
+    def worker(t):
+        for i in range(t, R, S):
+            H.hapi_extract(descs[t], packed, images[i * Q:(i + 1) * Q], Q, split, out[i])
+
+    def step():
+        th = [threading.Thread(target=worker, args=(t,)) for t in range(S)]
+        for x in th:
+            x.start()
+        for x in th:
+            x.join()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    print(json.dumps({
+        "metric": f"feature-extraction images/sec, {R} requests of {Q} images, "
+                  f"{S} in flight ({cfg['model']})",
+        "value": round(R * Q * args.steps / elapsed, 2), "unit": "images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(elapsed * 1e3 / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg["dtype"] == H.HAPI_BF16 else "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "requests": R, "request_images": Q,
+                   "concurrency": S, "chunk": chunk, "split_layer": split}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -87,9 +153,16 @@ def main():
     ap.add_argument("--workload", default="resnet50_bf16_b256")
     ap.add_argument("--batch", type=int, default=0, help="override the workload batch")
     ap.add_argument("--chunk", type=int, default=0)
+    ap.add_argument("--inflight", type=int, default=0,
+                    help="partitions in flight on separate streams (0: the library chooses)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="time the library's plain copy (split 0) instead, for counter calibration")
+    ap.add_argument("--concurrency", type=int, default=0,
+                    help="server mode: --requests requests of --request-images images per step, "
+                         "issued by this many host threads on as many streams")
+    ap.add_argument("--requests", type=int, default=8)
+    ap.add_argument("--request-images", type=int, default=128)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the extraction shards "
@@ -101,6 +174,9 @@ def main():
     from paper_2210_08650_amd import models as PM
     import synth
 
+    if args.concurrency:
+        return concurrent_requests(args)
+
     cfg = dict(PM.WORKLOADS[args.workload])
     if args.batch:
         cfg["batch"] = args.batch
@@ -109,7 +185,7 @@ def main():
     layers = PM.FACTORIES[cfg["model"]]()
     B = cfg["batch"]
     stream = torch.cuda.current_stream()
-    desc = H.Desc(layers, cfg["dtype"], stream=stream, chunk=args.chunk)
+    desc = H.Desc(layers, cfg["dtype"], stream=stream, chunk=args.chunk, inflight=args.inflight)
     tdt = torch.bfloat16 if cfg["dtype"] == H.HAPI_BF16 else torch.float32
 
     raw = torch.from_numpy(synth.flatten(synth.params(cfg["seed"], PM.raw_manifest(layers)))).cuda()
@@ -157,11 +233,16 @@ def main():
         achieved = c["bytes"] / (c["total_ms"] * 1e-3) / 1e9
         peak = HBM_PEAK
     else:
+        # Partitions in flight overlap their launches: the family's rate is its
+        # flops over the time at least one of its launches was running
+        # (equal to the summed durations when nothing overlaps).
         dom = fam[conv_name]
         bound, unit = "mfma", "TFLOP/s"
-        achieved = dom["flops"] / (dom["total_ms"] * 1e-3) / 1e12
+        achieved = dom["flops"] / (dom["busy_ms"] * 1e-3) / 1e12
         peak = PEAK[cfg["dtype_name"]]
-    mfma_util = None if args.calib_copy else round(100.0 * achieved / peak, 2)
+    # share of the whole step's MFMA capacity the convolutions used
+    mfma_util = None if args.calib_copy else round(
+        100.0 * dom["flops"] / args.steps / (ms_per_step * 1e-3) / 1e12 / peak, 2)
 
     default = args.workload == "resnet50_bf16_b256" and not args.batch and not args.calib_copy
     result = {
@@ -182,7 +263,8 @@ def main():
         "config": {"workload": args.workload + ("_copy_calibration" if args.calib_copy else ""),
                    "batch": B, "split_layer": split, "image": "3x224x224",
                    "chunk": args.chunk or "auto",
-                   "partitions": H.hapi_chunk_count(desc, B)},
+                   "partitions": H.hapi_chunk_count(desc, B),
+                   "inflight": args.inflight or "auto"},
         "mfma_util_pct": mfma_util,
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                      "frac": round(achieved / peak, 4),
@@ -191,8 +273,10 @@ def main():
                      "algorithmic_flops_per_launch": round(dom["flops"] / dom["launches"]),
                      "kernel": dom["name"], "launches_per_step": dom["launches"] // args.steps,
                      "avg_launch_us": round(dom["total_ms"] * 1e3 / dom["launches"], 2),
+                     "busy_us_per_launch": round(dom["busy_ms"] * 1e3 / dom["launches"], 2),
                      "share_of_kernel_time": round(dom["total_ms"] / total_kernel_ms, 4)},
         "kernel_families": {s["name"]: {"ms_per_step": round(s["total_ms"] / args.steps, 4),
+                                        "busy_ms_per_step": round(s["busy_ms"] / args.steps, 4),
                                         "launches_per_step": s["launches"] // args.steps}
                             for s in stats},
         "stats_pass_ms_per_step": round(stats_elapsed * 1e3 / args.steps, 4),

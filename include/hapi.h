@@ -14,9 +14,11 @@
  * Conventions shared by every entry point
  *  - Every data pointer is a DEVICE pointer owned by the caller (allocate with
  *    hipMalloc or as torch tensors), except the host arrays of
- *    hapi_layer_shape, hapi_profile_layers, hapi_stats_collect and
- *    hapi_choose_split.  The library never allocates or frees device memory
- *    except a few hipEvents for timing.
+ *    hapi_layer_shape, hapi_profile_layers, hapi_profile_memory,
+ *    hapi_stats_collect and hapi_choose_split.  The library never allocates
+ *    or frees device memory; it creates hipEvents for timing and, for
+ *    partitions in flight, up to 3 auxiliary streams per host thread and
+ *    device.
  *  - Return value: HAPI_OK (0) or a negative hapi_status.  The message of the
  *    last failure on the calling thread is returned by hapi_last_error().
  *    Every argument is validated before anything is launched, so a call that
@@ -125,8 +127,11 @@ typedef struct {
   void *stream;                       /* hipStream_t; NULL = the null stream */
   void *workspace;                    /* device scratch owned by the caller */
   size_t workspace_bytes;
-  int32_t chunk;                      /* storage-side (COS) batch: images per sequential
-                                         partition; 0 = the library chooses */
+  int32_t chunk;                      /* storage-side (COS) batch: images per partition;
+                                         0 = the library chooses */
+  int32_t inflight;                   /* partitions in flight at once, 0..4; 0 = the
+                                         library chooses: 2 when chunk == 0 and the
+                                         batch has >= 128 images, else 1 (sequential) */
 } hapi_model_desc;
 
 /* Raw (unpacked) weights: ONE flat float32 device buffer holding, layer by
@@ -179,11 +184,21 @@ int hapi_layer_shape(const hapi_model_desc *desc, int32_t layer, int64_t *dims, 
 int64_t hapi_workspace_bytes(const hapi_model_desc *desc, int32_t batch, int32_t split_layer,
                              int32_t profile);
 
-/* Number of sequential partitions (storage-side batches) hapi_extract uses for
- * `batch` images with desc->chunk (Storage-side batch size adaptation: a
- * request is processed as sequential partitions of the storage-side batch;
- * the last partition may be short).  Host only; < 0 on error. */
+/* Number of partitions (storage-side batches) hapi_extract uses for `batch`
+ * images with desc->chunk (Storage-side batch size adaptation: a request is
+ * processed as partitions of the storage-side batch; the last partition may
+ * be short).  Host only; < 0 on error. */
 int32_t hapi_chunk_count(const hapi_model_desc *desc, int32_t batch);
+
+/* Partitions in flight.  With k = min(inflight, partitions) > 1, partition p
+ * runs on lane p % k: lane 0 is desc->stream, lanes 1..k-1 are auxiliary
+ * streams (default priority) that the library creates once per host thread
+ * and device, forks from desc->stream at the start of the call and joins back
+ * into it at the end, so the call stays asynchronous and ordered on
+ * desc->stream.  Each lane has its own workspace slots (the workspace grows
+ * with k).  The paper's server runs up to 4 requests at once (Evaluation,
+ * Methodology); on this GPU partitions in flight overlap each other's layer
+ * ramps and tails.  Results do not depend on chunk or inflight. */
 
 /* The storage-side forward pass.
  *   weights      packed weights from hapi_pack_weights (same desc)
@@ -228,6 +243,14 @@ int hapi_extract_range(const hapi_model_desc *desc, const void *weights, const v
 int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out_bytes,
                         float *out_us);
 
+/* Per-split device memory (Measurement study, Fig. 2c: per-layer peak GPU
+ * memory).  bytes[k], k = 0..n_layers: every device byte a hapi_extract of
+ * `batch` images to split k uses with desc->chunk -- the packed weights of
+ * layers 1..k (a packed buffer for the first k layers is exactly that
+ * prefix), the images, the output and the workspace; the library allocates
+ * nothing else.  Host only, closed form, works without a GPU. */
+int hapi_profile_memory(const hapi_model_desc *desc, int32_t batch, int64_t *bytes);
+
 /* Per-kernel timing of later hapi_extract calls (for roofline reporting).
  * hapi_stats_enable(1) clears the counters and brackets every kernel launch of
  * hapi_extract with HIP events on desc->stream; hapi_stats_enable(0) stops.
@@ -237,9 +260,11 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
 typedef struct {
   char name[32];
   int64_t launches;
-  double total_ms;
+  double total_ms;    /* sum of the launches' durations */
   double flops;
   double bytes;
+  double busy_ms;     /* time at least one launch of the family was running (differs
+                         from total_ms when partitions in flight overlap) */
 } hapi_kernel_stat;
 
 int hapi_stats_enable(int32_t enable);

@@ -29,8 +29,8 @@ __all__ = ["HapiError", "Desc", "hapi_layer", "hapi_model_desc", "hapi_kernel_st
            "HAPI_BATCHNORM", "LIB_PATH", "EXPORTED",
            "hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
            "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-           "hapi_extract_range", "hapi_profile_layers", "hapi_stats_enable",
-           "hapi_stats_collect", "hapi_last_error", "hapi_split_job", "hapi_split_estimate", "hapi_split_choice", "hapi_choose_split"]
+           "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
+           "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error", "hapi_split_job", "hapi_split_estimate", "hapi_split_choice", "hapi_choose_split"]
 
 _STATUS = {HAPI_E_INVAL: "HAPI_E_INVAL", HAPI_E_UNSUPPORTED: "HAPI_E_UNSUPPORTED",
            HAPI_E_NOMEM: "HAPI_E_NOMEM", HAPI_E_DEVICE: "HAPI_E_DEVICE"}
@@ -55,13 +55,13 @@ class hapi_model_desc(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32),
                 ("in_w", ctypes.c_int32), ("stream", ctypes.c_void_p),
                 ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
-                ("chunk", ctypes.c_int32)]
+                ("chunk", ctypes.c_int32), ("inflight", ctypes.c_int32)]
 
 
 class hapi_kernel_stat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
-                ("bytes", ctypes.c_double)]
+                ("bytes", ctypes.c_double), ("busy_ms", ctypes.c_double)]
 
 
 class hapi_split_job(ctypes.Structure):
@@ -129,6 +129,7 @@ def _load():
         "hapi_extract_range": (ctypes.c_int, [D, vp, vp, i32, i32, i32, vp]),
         "hapi_profile_layers": (ctypes.c_int, [D, i32, ctypes.POINTER(i64),
                                                ctypes.POINTER(ctypes.c_float)]),
+        "hapi_profile_memory": (ctypes.c_int, [D, i32, ctypes.POINTER(i64)]),
         "hapi_stats_enable": (ctypes.c_int, [i32]),
         "hapi_stats_collect": (ctypes.c_int, [ctypes.POINTER(hapi_kernel_stat), i32]),
         "hapi_last_error": (ctypes.c_char_p, []),
@@ -145,8 +146,8 @@ def _load():
 _lib = _load()
 EXPORTED = ("hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
             "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-            "hapi_extract_range", "hapi_profile_layers", "hapi_stats_enable",
-            "hapi_stats_collect", "hapi_last_error", "hapi_choose_split")
+            "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
+            "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error", "hapi_choose_split")
 
 
 def _ptr(p):
@@ -175,7 +176,7 @@ class Desc:
     """Owns a ``hapi_model_desc`` and the layer array it points to."""
 
     def __init__(self, layers, dtype, in_shape=(3, 224, 224), stream=None, workspace=None,
-                 workspace_bytes=0, chunk=0):
+                 workspace_bytes=0, chunk=0, inflight=0):
         self._layers = (hapi_layer * len(layers))()
         for i, spec in enumerate(layers):
             if isinstance(spec, hapi_layer):
@@ -188,9 +189,10 @@ class Desc:
         self.c.layers = ctypes.cast(self._layers, ctypes.POINTER(hapi_layer))
         self.c.dtype = dtype
         self.c.in_c, self.c.in_h, self.c.in_w = in_shape
-        self.set(stream=stream, workspace=workspace, workspace_bytes=workspace_bytes, chunk=chunk)
+        self.set(stream=stream, workspace=workspace, workspace_bytes=workspace_bytes, chunk=chunk,
+                 inflight=inflight)
 
-    def set(self, stream=None, workspace=None, workspace_bytes=None, chunk=None):
+    def set(self, stream=None, workspace=None, workspace_bytes=None, chunk=None, inflight=None):
         if stream is not None:
             self.c.stream = _stream(stream)
         if workspace is not None:
@@ -199,6 +201,8 @@ class Desc:
             self.c.workspace_bytes = int(workspace_bytes)
         if chunk is not None:
             self.c.chunk = int(chunk)
+        if inflight is not None:
+            self.c.inflight = int(inflight)
         return self
 
     @property
@@ -257,6 +261,13 @@ def hapi_profile_layers(desc: Desc, batch: int, time_layers: bool = False):
     return [int(v) for v in b], ([float(v) for v in us] if us is not None else None)
 
 
+def hapi_profile_memory(desc: Desc, batch: int) -> list:
+    """Device bytes of an extraction to every split 0..n_layers."""
+    b = (ctypes.c_int64 * (desc.n_layers + 1))()
+    _check(_lib.hapi_profile_memory(desc.ref, int(batch), b))
+    return [int(v) for v in b]
+
+
 def hapi_stats_enable(enable: bool) -> None:
     _check(_lib.hapi_stats_enable(int(bool(enable))))
 
@@ -266,7 +277,8 @@ def hapi_stats_collect(max_entries: int = 16) -> list:
     n = _check(_lib.hapi_stats_collect(arr, max_entries))
     return [dict(name=arr[i].name.decode(), launches=int(arr[i].launches),
                  total_ms=float(arr[i].total_ms), flops=float(arr[i].flops),
-                 bytes=float(arr[i].bytes)) for i in range(min(n, max_entries))]
+                 bytes=float(arr[i].bytes), busy_ms=float(arr[i].busy_ms))
+            for i in range(min(n, max_entries))]
 
 
 def hapi_last_error() -> str:

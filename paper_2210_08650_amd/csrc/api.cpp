@@ -43,6 +43,8 @@ namespace {
 constexpr int64_t kAlign = 256;
 constexpr int64_t kIndexLimit = (int64_t)1 << 31;  // kernels index a partition with int32
 constexpr int kAutoChunk = 256;
+constexpr int kMaxInflight = 4;
+constexpr int kAutoInflightBatch = 128;
 
 int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -80,6 +82,7 @@ struct LayerPlan {
   std::vector<Extra> extras;
   bool has_sc = false;
   int64_t tmp_elems = 0;  // largest per-image tensor the layer reads or writes
+  int64_t pk_end = 0;     // packed-weight bytes of layers 1..this one
 };
 
 struct Model {
@@ -101,6 +104,8 @@ int analyze(const hapi_model_desc *d, Model &m) {
   if (d->in_c < 1 || d->in_h < 1 || d->in_w < 1)
     return fail(HAPI_E_INVAL, "bad input shape %dx%dx%d", d->in_c, d->in_h, d->in_w);
   if (d->chunk < 0) return fail(HAPI_E_INVAL, "chunk must be >= 0");
+  if (d->inflight < 0 || d->inflight > kMaxInflight)
+    return fail(HAPI_E_INVAL, "inflight must be in [0, %d]", kMaxInflight);
   m = Model();
   m.bf16 = d->dtype == HAPI_BF16;
   m.esz = m.bf16 ? 2 : 4;
@@ -341,6 +346,7 @@ int analyze(const hapi_model_desc *d, Model &m) {
     if (first && !m.first_reads_nchw && m.input.c % 8 != 0 && L.kind == HAPI_MAXPOOL)
       return fail(HAPI_E_UNSUPPORTED, "layer 1: max pooling needs channels %% 8 == 0");
     lp.tmp_elems = std::max({lp.tmp_elems, lp.in.elems(), lp.out.elems()});
+    lp.pk_end = pk;
     m.layers.push_back(lp);
     cur = lp.out;
   }
@@ -355,8 +361,20 @@ int64_t max_tmp(const Model &m, int split) {
   return t;
 }
 
+// Partitions in flight at once: the caller's choice, else two for a large
+// batch split automatically (one partition alone leaves each layer's ramp and
+// tail idle, and memory-bound layers of one partition overlap compute-bound
+// layers of the other), else one -- an explicit storage-side batch keeps the
+// paper's sequential partitions.
+int inflight_for(const hapi_model_desc *d, int batch) {
+  if (d->inflight > 0) return std::min(d->inflight, kMaxInflight);
+  return (d->chunk == 0 && batch >= kAutoInflightBatch) ? 2 : 1;
+}
+
 int chunk_for(const hapi_model_desc *d, const Model &m, int batch) {
-  int c = d->chunk > 0 ? std::min(d->chunk, batch) : std::min(batch, kAutoChunk);
+  const int lanes = inflight_for(d, batch);
+  int c = d->chunk > 0 ? std::min(d->chunk, batch)
+                       : std::min((batch + lanes - 1) / lanes, kAutoChunk);
   if (d->chunk == 0) {
     const int64_t per = std::max<int64_t>(1, max_tmp(m, (int)m.layers.size()));
     const int64_t lim = (kIndexLimit - 1) / per;
@@ -369,8 +387,14 @@ int64_t slot_bytes(const Model &m, int split, int chunk) {
   return align_up((int64_t)chunk * max_tmp(m, split) * m.esz);
 }
 
-int64_t workspace_for(const Model &m, int split, int chunk, bool profile, int batch) {
-  int64_t b = split > 0 ? 3 * slot_bytes(m, split, chunk) : 0;
+// Streams a batch actually uses: no more than it has partitions.
+int lanes_for(const hapi_model_desc *d, int chunk, int batch) {
+  return std::max(1, std::min(inflight_for(d, batch), (batch + chunk - 1) / chunk));
+}
+
+// Three activation slots per partition in flight (profiling runs one).
+int64_t workspace_for(const Model &m, int split, int chunk, bool profile, int batch, int lanes) {
+  int64_t b = split > 0 ? (profile ? 1 : lanes) * 3 * slot_bytes(m, split, chunk) : 0;
   if (profile) b += align_up(m.packed_bytes) + align_up((int64_t)batch * m.input.elems() * m.esz);
   return b;
 }
@@ -796,21 +820,74 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
   return HAPI_OK;
 }
 
+// Auxiliary streams of one host thread on one device, with the events that
+// fork them from the caller's stream and join them back.  Created on first
+// use and kept for the thread's lifetime; per thread, so that concurrent
+// callers never record each other's events.
+struct Lanes {
+  int dev = -1;
+  hipStream_t aux[kMaxInflight - 1] = {};
+  hipEvent_t fork = nullptr, join[kMaxInflight - 1] = {};
+};
+
+int get_lanes(hipStream_t s, Lanes **out) {
+  static thread_local std::vector<Lanes> per_dev;
+  int dev = 0, cur = 0;
+  HIP_TRY(hipStreamGetDevice(s, &dev));
+  HIP_TRY(hipGetDevice(&cur));
+  if (dev != cur) return fail(HAPI_E_INVAL, "desc->stream belongs to device %d, current device is %d", dev, cur);
+  if ((int)per_dev.size() <= dev) per_dev.resize(dev + 1);
+  Lanes &L = per_dev[dev];
+  if (L.dev < 0) {
+    HIP_TRY(hipEventCreateWithFlags(&L.fork, hipEventDisableTiming));
+    for (int i = 0; i < kMaxInflight - 1; ++i) {
+      HIP_TRY(hipStreamCreateWithFlags(&L.aux[i], hipStreamNonBlocking));
+      HIP_TRY(hipEventCreateWithFlags(&L.join[i], hipEventDisableTiming));
+    }
+    L.dev = dev;
+  }
+  *out = &L;
+  return HAPI_OK;
+}
+
+// Runs the batch as partitions of `chunk` images, `lanes` of them in flight:
+// partition p runs on lane p % lanes (lane 0 is desc->stream, the others
+// auxiliary streams forked from it and joined back into it at the end) with
+// that lane's three workspace slots.  Partitions are independent, and each
+// gives the same bits whichever lane runs it.
 int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, const void *images,
-              int batch, int start, int split, void *out, uint8_t *ws, int chunk,
+              int batch, int start, int split, void *out, uint8_t *ws, int chunk, int lanes,
               const std::function<void(int, bool)> &on_layer) {
   hipStream_t s = static_cast<hipStream_t>(d->stream);
   const int64_t sb = slot_bytes(m, split, chunk);
-  Ctx c{m, s, static_cast<const uint8_t *>(weights), {ws, ws + sb, ws + 2 * sb}, on_layer};
+  Lanes *L = nullptr;
+  if (lanes > 1) {
+    if (int r = get_lanes(s, &L)) return r;
+    HIP_TRY(hipEventRecord(L->fork, s));
+    for (int i = 1; i < lanes; ++i) HIP_TRY(hipStreamWaitEvent(L->aux[i - 1], L->fork, 0));
+  }
+  std::vector<Ctx> c;
+  c.reserve(lanes);
+  for (int i = 0; i < lanes; ++i) {
+    uint8_t *w0 = ws + (int64_t)i * 3 * sb;
+    c.push_back(Ctx{m, i ? L->aux[i - 1] : s, static_cast<const uint8_t *>(weights),
+                    {w0, w0 + sb, w0 + 2 * sb}, on_layer});
+  }
   const int64_t in_bytes = act_at(m, start).elems() * m.esz;
   const int64_t out_bytes = m.layers[split - 1].out.elems() * m.esz;
-  for (int b0 = 0; b0 < batch; b0 += chunk) {
+  int r = HAPI_OK;
+  for (int b0 = 0, p = 0; b0 < batch && r == HAPI_OK; b0 += chunk, ++p) {
     const int nb = std::min(chunk, batch - b0);
-    const int r = run_chunk(c, static_cast<const uint8_t *>(images) + (int64_t)b0 * in_bytes, nb, start,
-                            split, out ? static_cast<uint8_t *>(out) + (int64_t)b0 * out_bytes : nullptr);
-    if (r != HAPI_OK) return r;
+    r = run_chunk(c[p % lanes], static_cast<const uint8_t *>(images) + (int64_t)b0 * in_bytes, nb, start,
+                  split, out ? static_cast<uint8_t *>(out) + (int64_t)b0 * out_bytes : nullptr);
   }
-  return HAPI_OK;
+  // Join even after a failed launch, so that desc->stream still orders
+  // everything that was issued.
+  for (int i = 1; i < lanes; ++i) {
+    HIP_TRY(hipEventRecord(L->join[i - 1], L->aux[i - 1]));
+    HIP_TRY(hipStreamWaitEvent(s, L->join[i - 1], 0));
+  }
+  return r;
 }
 
 }  // namespace
@@ -868,7 +945,7 @@ int64_t hapi_workspace_bytes(const hapi_model_desc *desc, int32_t batch, int32_t
   const int chunk = chunk_for(desc, m, batch);
   if ((int64_t)chunk * max_tmp(m, split_layer) >= kIndexLimit)
     return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
-  return workspace_for(m, split_layer, chunk, profile != 0, batch);
+  return workspace_for(m, split_layer, chunk, profile != 0, batch, lanes_for(desc, chunk, batch));
 }
 
 int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void *packed) {
@@ -937,13 +1014,14 @@ int extract_range(const hapi_model_desc *desc, const void *weights, const void *
   const int chunk = chunk_for(desc, m, batch);
   if ((int64_t)chunk * max_tmp(m, split_layer) >= kIndexLimit)
     return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
-  const int64_t need = workspace_for(m, split_layer, chunk, false, batch);
+  const int lanes = lanes_for(desc, chunk, batch);
+  const int64_t need = workspace_for(m, split_layer, chunk, false, batch, lanes);
   if (!desc->workspace || (int64_t)desc->workspace_bytes < need)
     return fail(HAPI_E_NOMEM, "workspace of %zu bytes, %lld needed", desc->workspace_bytes,
                 (long long)need);
   if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
   return run_batch(desc, m, weights, images, batch, start_layer, split_layer, out,
-                   static_cast<uint8_t *>(desc->workspace), chunk, nullptr);
+                   static_cast<uint8_t *>(desc->workspace), chunk, lanes, nullptr);
 }
 
 }  // namespace
@@ -958,6 +1036,25 @@ int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *i
 int hapi_extract_range(const hapi_model_desc *desc, const void *weights, const void *input,
                        int32_t batch, int32_t start_layer, int32_t end_layer, void *out) {
   return extract_range(desc, weights, input, batch, start_layer, end_layer, out);
+}
+
+int hapi_profile_memory(const hapi_model_desc *desc, int32_t batch, int64_t *bytes) {
+  Model m;
+  const int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (batch < 1) return fail(HAPI_E_INVAL, "batch must be >= 1");
+  if (!bytes) return fail(HAPI_E_INVAL, "bytes is NULL");
+  const int n = (int)m.layers.size();
+  const int chunk = chunk_for(desc, m, batch);
+  if ((int64_t)chunk * max_tmp(m, n) >= kIndexLimit)
+    return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
+  const int64_t images = (int64_t)batch * m.input.elems() * m.esz;
+  for (int k = 0; k <= n; ++k) {
+    const int64_t weights = k == 0 ? 0 : m.layers[k - 1].pk_end;
+    const int64_t out = (int64_t)batch * act_at(m, k).elems() * m.esz;
+    bytes[k] = weights + images + out + workspace_for(m, k, chunk, false, batch, lanes_for(desc, chunk, batch));
+  }
+  return HAPI_OK;
 }
 
 int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out_bytes,
@@ -977,7 +1074,7 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
   const int chunk = chunk_for(desc, m, batch);
   if ((int64_t)chunk * max_tmp(m, n) >= kIndexLimit)
     return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
-  const int64_t need = workspace_for(m, n, chunk, true, batch);
+  const int64_t need = workspace_for(m, n, chunk, true, batch, 1);
   if (!desc->workspace || (int64_t)desc->workspace_bytes < need)
     return fail(HAPI_E_NOMEM, "workspace of %zu bytes, %lld needed", desc->workspace_bytes,
                 (long long)need);
@@ -1016,7 +1113,7 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
       (void)begin;
       (void)hipEventRecord(ev[idx++], s);
     };
-    rc = run_batch(desc, m, pk, img, batch, 0, n, nullptr, ws, chunk, cb);
+    rc = run_batch(desc, m, pk, img, batch, 0, n, nullptr, ws, chunk, 1, cb);
     if (rc != HAPI_OK) break;
     if (hipEventSynchronize(ev[idx - 1]) != hipSuccess) {
       rc = fail(HAPI_E_DEVICE, "hipEventSynchronize failed");
@@ -1060,14 +1157,35 @@ int hapi_stats_collect(hapi_kernel_stat *out, int32_t max_entries) {
   hapi_kernel_stat acc[F_COUNT];
   std::memset(acc, 0, sizeof acc);
   for (int f = 0; f < F_COUNT; ++f) std::snprintf(acc[f].name, sizeof acc[f].name, "%s", kFamily[f]);
+  // Launch intervals relative to the first recorded start, per family, for
+  // the time at least one launch of the family was running (launches of
+  // partitions in flight on different streams overlap).
+  std::vector<std::pair<float, float>> iv[F_COUNT];
   for (StatRec &r : g_recs) {
     if (hipEventSynchronize(r.b) != hipSuccess) return fail(HAPI_E_DEVICE, "hipEventSynchronize failed");
-    float ms = 0.0f;
+    float ms = 0.0f, t0 = 0.0f;
     (void)hipEventElapsedTime(&ms, r.a, r.b);
+    (void)hipEventElapsedTime(&t0, g_recs.front().a, r.a);
     acc[r.fam].launches += 1;
     acc[r.fam].total_ms += ms;
     acc[r.fam].flops += r.flops;
     acc[r.fam].bytes += r.bytes;
+    iv[r.fam].emplace_back(t0, t0 + ms);
+  }
+  for (int f = 0; f < F_COUNT; ++f) {
+    std::sort(iv[f].begin(), iv[f].end());
+    double busy = 0.0, lo = 0.0, hi = -1e30;
+    for (const auto &x : iv[f]) {
+      if (x.first > hi) {
+        if (hi > lo) busy += hi - lo;
+        lo = x.first;
+        hi = x.second;
+      } else {
+        hi = std::max(hi, (double)x.second);
+      }
+    }
+    if (!iv[f].empty() && hi > lo) busy += hi - lo;
+    acc[f].busy_ms = busy;
   }
   int nout = 0;
   for (int f = 0; f < F_COUNT; ++f) {

@@ -43,7 +43,8 @@ class Runner:
         self.desc = H.Desc(layers, dtype, in_shape, stream=self.stream)
         raw = torch.from_numpy(synth.flatten(params)).cuda()
         assert raw.numel() == H.hapi_raw_weight_count(self.desc)
-        self.packed = torch.empty(max(H.hapi_packed_weight_bytes(self.desc), 256),
+        # zeroed, so that the alignment gaps the packer skips compare equal
+        self.packed = torch.zeros(max(H.hapi_packed_weight_bytes(self.desc), 256),
                                   dtype=torch.uint8, device="cuda")
         H.hapi_pack_weights(self.desc, raw if raw.numel() else None, self.packed)
         torch.cuda.synchronize()
@@ -53,9 +54,9 @@ class Runner:
     def out_shape(self, split):
         return H.hapi_layer_shape(self.desc, split)
 
-    def extract(self, images_dev, split, chunk=0, workspace_pad=0, out=None):
+    def extract(self, images_dev, split, chunk=0, workspace_pad=0, out=None, inflight=0):
         batch = images_dev.shape[0]
-        self.desc.set(chunk=chunk)
+        self.desc.set(chunk=chunk, inflight=inflight)
         need = H.hapi_workspace_bytes(self.desc, batch, split)
         ws = torch.empty(max(need + workspace_pad, 256), dtype=torch.uint8, device="cuda")
         self.desc.set(workspace=ws, workspace_bytes=need + workspace_pad)
@@ -65,10 +66,10 @@ class Runner:
         torch.cuda.synchronize()
         return out
 
-    def resume(self, input_dev, start, end, chunk=0):
+    def resume(self, input_dev, start, end, chunk=0, inflight=0):
         """Layers start+1..end on the layer-``start`` tensor (caller layout)."""
         batch = input_dev.shape[0]
-        self.desc.set(chunk=chunk)
+        self.desc.set(chunk=chunk, inflight=inflight)
         need = H.hapi_workspace_bytes(self.desc, batch, end)
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device="cuda")
         self.desc.set(workspace=ws, workspace_bytes=need)
@@ -77,5 +78,5 @@ class Runner:
         torch.cuda.synchronize()
         return out
 
-    def extract_np(self, images_dev, split, chunk=0):
-        return self.extract(images_dev, split, chunk).float().cpu().numpy()
+    def extract_np(self, images_dev, split, chunk=0, inflight=0):
+        return self.extract(images_dev, split, chunk, inflight=inflight).float().cpu().numpy()

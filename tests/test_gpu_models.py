@@ -55,8 +55,10 @@ def test_chunking_is_bit_exact(name, split, chunks):
     r, _, _, xd, _, _ = _setup(name, 40, 5)
     whole = r.extract_np(xd, split, chunk=0)
     for c in chunks:
-        assert H.hapi_chunk_count(r.desc.set(chunk=c), 5) == -(-5 // c)
+        assert H.hapi_chunk_count(r.desc.set(chunk=c, inflight=0), 5) == -(-5 // c)
         assert np.array_equal(r.extract_np(xd, split, chunk=c), whole), c
+        for k in (2, 3, 4):  # partitions in flight on several streams
+            assert np.array_equal(r.extract_np(xd, split, chunk=c, inflight=k), whole), (c, k)
     # row i depends on image i only
     single = r.extract_np(xd[3:4].contiguous(), split)
     assert np.array_equal(single[0], whole[3])
@@ -246,6 +248,7 @@ def test_resume_from_split_is_bit_exact(name, pairs):
         assert torch.equal(got, whole), (s, e)
         if s < e:
             assert torch.equal(r.resume(mid, s, e, chunk=2), whole), (s, e)
+            assert torch.equal(r.resume(mid, s, e, chunk=1, inflight=3), whole), (s, e)
 
 
 @pytest.mark.parametrize("name,s,e", [("resnet50", 5, 12), ("alexnet", 3, 8),
@@ -261,3 +264,57 @@ def test_resume_matches_oracle(name, s, e):
     err = rel_l2(got, ref)
     print(f"{name}: resume {s} -> {e} rel_l2 {err:.3e}", flush=True)
     assert got.shape == ref.shape and err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("name", ["resnet50", "vit_b16", "densenet121"])
+def test_packed_prefix_serves_a_truncated_model(name):
+    """The memory profile counts the packed weights of layers 1..k as a prefix
+    of the full packed buffer: packing only the first k layers gives exactly
+    those bytes, and extracting with them gives the same split output."""
+    r, om, ps, xd, _, dtype = _setup(name, 94, 2)
+    k = om.n_layers // 2
+    counts = om.param_counts()
+    short = Runner(PM.FACTORIES[name]()[:k], dtype, ps[:sum(counts[:k])])
+    n = H.hapi_packed_weight_bytes(short.desc)
+    assert torch.equal(short.packed[:n], r.packed[:n])
+    assert torch.equal(short.extract(xd, k), r.extract(xd, k))
+
+
+@pytest.mark.parametrize("streams", [2, 4])
+def test_concurrent_requests_match_sequential(streams):
+    """Requests issued from several host threads onto separate streams, each
+    with its own workspace (the server's concurrent requests), give the same
+    bits as one after another."""
+    import threading
+    r, _, _, _, _, dtype = _setup("resnet50", 95, 1)
+    reqs = 8
+    imgs = torch.from_numpy(synth.images(95, reqs * 16)).to(torch.bfloat16).cuda()
+    layers = PM.resnet50()
+    seq = torch.stack([r.extract(imgs[i * 16:(i + 1) * 16].contiguous(), 18, chunk=4)
+                       for i in range(reqs)])
+    out = torch.empty_like(seq)
+    side = [torch.cuda.Stream() for _ in range(streams)]
+    descs, spaces = [], []
+    for t in range(streams):
+        d = H.Desc(layers, dtype, stream=side[t], chunk=4)
+        need = H.hapi_workspace_bytes(d, 16, 18)
+        spaces.append(torch.empty(need, dtype=torch.uint8, device="cuda"))
+        descs.append(d.set(workspace=spaces[t], workspace_bytes=need))
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(t):
+        try:
+            for i in range(t, reqs, streams):
+                H.hapi_extract(descs[t], r.packed, imgs[i * 16:(i + 1) * 16], 16, 18, out[i])
+        except Exception as e:  # reported below; the GPU work already issued drains
+            errors.append(e)
+
+    th = [threading.Thread(target=worker, args=(t,)) for t in range(streams)]
+    for x in th:
+        x.start()
+    for x in th:
+        x.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    assert torch.equal(out, seq)

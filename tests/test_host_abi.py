@@ -91,6 +91,12 @@ def test_chunk_plan_matches_paper_example():
     assert H.hapi_chunk_count(d, 130) == 9       # short tail partition
     d.set(chunk=0)
     assert H.hapi_chunk_count(d, 64) == 1
+    # automatic partitioning: two halves in flight from 128 images on
+    assert H.hapi_chunk_count(d, 256) == 2 and H.hapi_chunk_count(d, 127) == 1
+    assert H.hapi_chunk_count(d, 1000) == 4                 # 500 per lane, capped at 256
+    assert H.hapi_chunk_count(d.set(inflight=1), 256) == 1
+    assert H.hapi_chunk_count(d.set(inflight=4), 256) == 4
+    d.set(inflight=0)
 
 
 @pytest.mark.parametrize("name", NAMES)
@@ -105,6 +111,35 @@ def test_workspace_covers_memory_estimate(name):
         assert H.hapi_workspace_bytes(d, 128, split) >= est
     assert H.hapi_workspace_bytes(d, 128, 0) == 0
     assert H.hapi_workspace_bytes(d, 128, om.n_layers, True) > H.hapi_workspace_bytes(d, 128, om.n_layers)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_memory_profile_is_every_buffer_of_an_extraction(name):
+    layers = PM.FACTORIES[name]()
+    dt = H.HAPI_F32 if name == "alexnet" else H.HAPI_BF16
+    d = H.Desc(layers, dt, chunk=16)
+    mem = H.hapi_profile_memory(d, 128)
+    out, _ = H.hapi_profile_layers(d, 128)
+    for k in range(d.n_layers + 1):
+        weights = H.hapi_packed_weight_bytes(H.Desc(layers[:k], dt)) if k else 0
+        assert mem[k] == weights + out[0] + out[k] + H.hapi_workspace_bytes(d, 128, k), k
+        if k:  # at least the paper's estimate for the partition batch
+            assert mem[k] - weights - out[0] - out[k] >= max(
+                out[j - 1] + out[j] for j in range(1, k + 1)) // 8
+
+
+def test_workspace_holds_one_slot_set_per_partition_in_flight():
+    d = _desc("resnet50", chunk=16)
+    one = H.hapi_workspace_bytes(d, 128, 18)
+    for k in (2, 3, 4):
+        assert H.hapi_workspace_bytes(d.set(inflight=k), 128, 18) == k * one
+    assert H.hapi_workspace_bytes(d.set(inflight=4), 32, 18) == 2 * one  # only 2 partitions
+    # automatic: 2 x 128-image partitions need what 1 x 256 needs
+    auto = _desc("resnet50")
+    seq = _desc("resnet50", chunk=256)
+    assert H.hapi_workspace_bytes(auto, 256, 18) == H.hapi_workspace_bytes(seq, 256, 18)
+    _raises(H.HAPI_E_INVAL, H.hapi_workspace_bytes, d.set(inflight=5), 128, 18)
+    _raises(H.HAPI_E_INVAL, H.hapi_workspace_bytes, d.set(inflight=-1), 128, 18)
 
 
 def _raises(code, fn, *a):
