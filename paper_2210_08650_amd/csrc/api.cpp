@@ -467,10 +467,21 @@ struct Ctx {
   std::function<void(int, bool)> on_layer;  // (layer index, begin) for profiling
 };
 
+// Per-channel scale and shift (an inference batch-norm) that a 1 x 1
+// convolution applies with ReLU to its input as it reads it; lda: the input's
+// row stride when it is a channel prefix of a wider tensor.
+struct PreAct {
+  const float *scale = nullptr, *shift = nullptr;
+  int lda = 0;
+};
+
 hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &in, int nb,
                     void *y, const void *res, bool relu, bool gelu, bool nchw_input, int ldc = 0,
-                    const void *x2 = nullptr, const Act *in2 = nullptr) {
+                    const void *x2 = nullptr, const Act *in2 = nullptr, PreAct pre = PreAct{}) {
   ConvArgs a{};
+  a.pre_scale = pre.scale;
+  a.pre_shift = pre.shift;
+  a.lda = pre.lda;
   a.x = x;
   a.w = c.pk + cs.pk_w;
   a.bias = reinterpret_cast<const float *>(c.pk + cs.pk_b);
@@ -744,16 +755,22 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
       }
       case HAPI_PREACT_CONV: {
         // Batch-norm + ReLU in front of the convolution cannot fold into its
-        // weights; it runs on the input, then the plain convolution.
+        // weights.  A 1 x 1 convolution applies them to its operand as it
+        // reads it; otherwise they run on the input first.
         const int A = free_slot(), B = free_slot(A);
         const int64_t pixels = (int64_t)nb * lp.in.h * lp.in.w;
         const Extra &bn = lp.extras[0];
-        HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * lp.in.c, 2.0 * pixels * lp.in.c * m.esz, [&] {
-          return launch_affine(cur, reinterpret_cast<const float *>(c.pk + bn.pk),
-                               reinterpret_cast<const float *>(c.pk + bn.pk) + bn.n, c.slot[A], pixels,
-                               lp.in.c, lp.in.c, true, c.s);
-        }));
-        HIP_TRY(run_conv(c, lp.convs[0], c.slot[A], lp.in, nb, c.slot[B], nullptr, false, false, false));
+        const float *scale = reinterpret_cast<const float *>(c.pk + bn.pk), *shift = scale + bn.n;
+        const ConvSpec &cs = lp.convs[0];
+        if (cs.k == 1 && cs.stride == 1 && cs.pad == 0 && cs.K <= kPreMax) {
+          HIP_TRY(run_conv(c, cs, cur, lp.in, nb, c.slot[B], nullptr, false, false, false, 0, nullptr, nullptr,
+                           PreAct{scale, shift, 0}));
+        } else {
+          HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * lp.in.c, 2.0 * pixels * lp.in.c * m.esz, [&] {
+            return launch_affine(cur, scale, shift, c.slot[A], pixels, lp.in.c, lp.in.c, true, c.s);
+          }));
+          HIP_TRY(run_conv(c, cs, c.slot[A], lp.in, nb, c.slot[B], nullptr, false, false, false));
+        }
         cur = c.slot[B];
         cur_slot = B;
         break;
@@ -786,14 +803,20 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         for (size_t l = 0; l < lp.extras.size(); ++l) {
           const int ch = lp.in.c + (int)l * growth;
           const Extra &bn = lp.extras[l];
-          HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * ch, 2.0 * pixels * ch * m.esz, [&] {
-            return launch_affine(cat, reinterpret_cast<const float *>(c.pk + bn.pk),
-                                 reinterpret_cast<const float *>(c.pk + bn.pk) + bn.n, c.slot[H], pixels,
-                                 ch, cout, true, c.s);
-          }));
+          const float *scale = reinterpret_cast<const float *>(c.pk + bn.pk), *shift = scale + bn.n;
           const Act hin{ch, lp.in.h, lp.in.w, false};
           const Act tin{bott, lp.in.h, lp.in.w, false};
-          HIP_TRY(run_conv(c, lp.convs[2 * l], c.slot[H], hin, nb, c.slot[B], nullptr, true, false, false));
+          // The 1 x 1 convolution reads the first ch channels of the
+          // concatenation and applies BN1 + ReLU as it reads them.
+          if (ch <= kPreMax) {
+            HIP_TRY(run_conv(c, lp.convs[2 * l], cat, hin, nb, c.slot[B], nullptr, true, false, false, 0, nullptr,
+                             nullptr, PreAct{scale, shift, cout}));
+          } else {
+            HIP_TRY(timed(c.s, F_AFFINE, 2.0 * pixels * ch, 2.0 * pixels * ch * m.esz, [&] {
+              return launch_affine(cat, scale, shift, c.slot[H], pixels, ch, cout, true, c.s);
+            }));
+            HIP_TRY(run_conv(c, lp.convs[2 * l], c.slot[H], hin, nb, c.slot[B], nullptr, true, false, false));
+          }
           HIP_TRY(run_conv(c, lp.convs[2 * l + 1], c.slot[B], tin, nb, cat + (int64_t)ch * m.esz, nullptr,
                            false, false, false, cout));
         }

@@ -66,7 +66,7 @@ __device__ __forceinline__ RowState make_row(const ConvArgs &a, int m) {
     return r;
   }
   if (LD == LD_GEMM) {
-    r.base = m * a.K; r.hi0 = 0; r.wi0 = 0;
+    r.base = m * (a.lda ? a.lda : a.K); r.hi0 = 0; r.wi0 = 0;
     return r;
   }
   const int hw = a.Ho * a.Wo;
@@ -419,7 +419,20 @@ struct PipeSmem {
 // swapped (weights as A, activations as B) so each lane's accumulators hold 4
 // consecutive output channels of one output pixel; the epilogue stores them
 // directly as 8-byte writes and the kernel needs no LDS beyond the stages.
-template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED, int EPI>
+// ReLU(x * scale + shift) on 8 consecutive channels, rounded to bf16 once.
+__device__ __forceinline__ bf16x8_t preact8(bf16x8_t v, float4 s0, float4 s1, float4 h0, float4 h1) {
+  typedef float f32x8_t __attribute__((ext_vector_type(8)));
+  f32x8_t f = __builtin_convertvector(v, f32x8_t);
+  const float sc[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+  const float sh[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f[e] = fmaxf(__builtin_fmaf(f[e], sc[e], sh[e]), 0.0f);
+  return __builtin_convertvector(f, bf16x8_t);
+}
+
+// PRE: the A operand is pre-activated (ConvArgs::pre_scale) between LDS and
+// the MFMAs; the per-channel scale and shift are staged in LDS once.
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED, int EPI, bool PRE = false>
 __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a) {
   constexpr int NT = WM * WN * 64;                    // threads: WM x WN waves
   constexpr int TM = BM / (WM * 32), TN = BN / (WN * 32);
@@ -431,12 +444,21 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   static_assert((STAGES - 2) * (NA + NB) < 64, "vmcnt range");
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[SM::kBytes];
   uint16_t *smem = reinterpret_cast<uint16_t *>(smem_raw);
+  __shared__ __attribute__((aligned(16))) float pre_s[PRE ? 2 * kPreMax : 4];
 
   const int tiles_n = (a.N + BN - 1) / BN;
   const int tile = xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  if constexpr (PRE) {
+    // Zero beyond K: the padded k columns read zeros and stay zero.
+    for (int c = t; c < a.Kp; c += NT) {
+      pre_s[c] = c < a.K ? a.pre_scale[c] : 0.0f;
+      pre_s[kPreMax + c] = c < a.K ? a.pre_shift[c] : 0.0f;
+    }
+    __syncthreads();
+  }
   DmaPlan<NA, NB, LD> dp;
   dp.init(a, m0, n0, wave * NA, wave * NB, lane);
   const int nk = a.Kp / BK;
@@ -490,12 +512,21 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     if (st < nk) issue(st, st, 0, NA + NB);
 
   bf16x8_t af[2][TM], bfr[2][TN];
-  auto read_frags = [&](const uint16_t *S, int ks, int buf) {
+  auto read_frags = [&](const uint16_t *S, int ks, int buf, int kt) {
     const int ch = ((2 * ks + lh) ^ sw) * 8;
 #pragma unroll
     for (int i = 0; i < TM; ++i) af[buf][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
 #pragma unroll
     for (int j = 0; j < TN; ++j) bfr[buf][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
+    if constexpr (PRE) {
+      // this lane's 8 channels: logical chunk 2 ks + lh of k-tile kt
+      const float *ps = pre_s + kt * BK + (2 * ks + lh) * 8;
+      const float4 s0 = *reinterpret_cast<const float4 *>(ps), s1 = *reinterpret_cast<const float4 *>(ps + 4);
+      const float4 h0 = *reinterpret_cast<const float4 *>(ps + kPreMax);
+      const float4 h1 = *reinterpret_cast<const float4 *>(ps + kPreMax + 4);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[buf][i] = preact8(af[buf][i], s0, s1, h0, h1);
+    }
   };
   // One k-tile from LDS stage S: KS MFMA k-steps; step ks reads the
   // fragments of step ks + 1 while its MFMAs run.  With a DMA (WITH_DMA), the
@@ -506,14 +537,14 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   // With SCHED each step is its own scheduling region in which the reads and
   // DMA issues are placed between the MFMAs, so one wait per step covers the
   // next step's operands.
-  auto run_tile = [&](const uint16_t *S, int kn, int sn, auto with_dma) {
+  auto run_tile = [&](const uint16_t *S, int kc, int kn, int sn, auto with_dma) {
     constexpr bool WITH_DMA = decltype(with_dma)::value;
-    read_frags(S, 0, 0);
+    read_frags(S, 0, 0, kc);
     if (SCHED) __builtin_amdgcn_sched_barrier(0);
     static_for<KS>([&](auto ksc) {
       constexpr int ks = decltype(ksc)::value;
       constexpr int cur = ks & 1;
-      if constexpr (ks + 1 < KS) read_frags(S, ks + 1, cur ^ 1);
+      if constexpr (ks + 1 < KS) read_frags(S, ks + 1, cur ^ 1, kc);
       constexpr int NDS = KS > 1 ? KS - 1 : 1, NQ = NA + NB;
       constexpr int q0 = !WITH_DMA || ks >= NDS ? 0 : ks * NQ / NDS;
       constexpr int q1 = !WITH_DMA || ks >= NDS ? 0 : (ks + 1) * NQ / NDS;
@@ -539,14 +570,14 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     wait_vmcnt<(STAGES - 2) * (NA + NB)>();
     __builtin_amdgcn_s_barrier();
     const int kn = kt + STAGES - 1;
-    run_tile(smem + (kt % STAGES) * SM::kStage, kn, kn % STAGES, std::true_type{});
+    run_tile(smem + (kt % STAGES) * SM::kStage, kt, kn, kn % STAGES, std::true_type{});
   }
   // Drain: no more tiles to issue.
   for (; kt < nk; ++kt) {
     if (STAGES >= 3 && nk - 1 - kt >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * (NA + NB)>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    run_tile(smem + (kt % STAGES) * SM::kStage, 0, 0, std::false_type{});
+    run_tile(smem + (kt % STAGES) * SM::kStage, kt, 0, 0, std::false_type{});
   }
   if (EPI) {
     // acc[i][j][4g + e] = C[m][n + e], m = block row + lane % 32,
@@ -992,10 +1023,10 @@ hipError_t launch_bf16_cfg(const ConvArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED = 1, int EPI = 0>
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED = 1, int EPI = 0, bool PRE = false>
 hipError_t launch_pipe_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hapi_launch((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED, EPI>), dim3(tiles),
+  hapi_launch((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED, EPI, PRE>), dim3(tiles),
                      dim3(WM * WN * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -1743,6 +1774,9 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     case 45: return launch_pws_ld<256, 64, 4, 1, 4, 3, LD, 2>(a, s);
     case 46: return launch_pws_ld<256, 64, 8, 1, 4, 3, LD, 2>(a, s);
     case 47: return launch_pws_ld<256, 128, 4, 2, 4, 2, LD, 2>(a, s);
+    case 48: return launch_pws_ld<128, 256, 2, 2, 4, 3, LD, 2>(a, s);
+    case 49: return launch_pws_ld<256, 128, 2, 2, 4, 3, LD, 2>(a, s);
+    case 56: return launch_pws_ld<128, 256, 2, 2, 2, 3, LD, 2>(a, s);
     case 50: if (a.Kp <= 2 * BK) return launch_short_ld<128, 128, 2, 2, LD, 3>(a, s); break;
     case 51: if (a.Kp <= 2 * BK) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s); break;
     case 52: if (a.Kp <= 2 * BK) return launch_short_ld<64, 128, 2, 2, LD, 4>(a, s); break;
@@ -1998,6 +2032,16 @@ hipError_t launch_stream(const ConvArgs &a, Loader ld, hipStream_t s) {
 }
 
 hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
+  if (a.pre_scale || (a.lda && a.lda != a.K)) {
+    // Pre-activated or strided A (a channel prefix of a wider tensor): the
+    // pipelined kernel, whose loader zero-fills the ragged last k-tile.
+    if (ld != LD_GEMM || a.N % 8 || a.ldc % 8 || a.ldr % 8 || a.K % 8 || a.lda % 8 || a.Kp > kPreMax ||
+        (a.lda && a.lda < a.K) || (int64_t)a.M * (a.lda ? a.lda : a.K) * 2 >= ((int64_t)1 << 31))
+      return hipErrorInvalidValue;
+    if (!a.pre_scale) return launch_pipe_cfg<128, 128, 2, 2, 2, LD_GEMM, 1, 0>(a, s);
+    if (a.N <= 64) return launch_pipe_cfg<128, 64, 2, 2, 3, LD_GEMM, 1, 0, true>(a, s);
+    return launch_pipe_cfg<128, 128, 2, 2, 2, LD_GEMM, 1, 0, true>(a, s);
+  }
   if (launch_stream(a, ld, s) == hipSuccess) return hipSuccess;
   switch (ld) {
     // The pipelined kernel needs 16-byte output rows; the register-staged one

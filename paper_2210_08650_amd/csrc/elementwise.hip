@@ -104,6 +104,39 @@ __global__ void avgpool_kernel(const T *__restrict__ x, T *__restrict__ y, int n
   Elt<T>::st(y, i, s / (float)(kh * kw));
 }
 
+// bf16 NHWC with C % 8 == 0: 8 channels per thread, 16-byte loads and
+// stores; the same summation order and rounding as avgpool_kernel.
+__global__ void avgpool8_kernel(const uint16_t *__restrict__ x, uint16_t *__restrict__ y, int n, int H,
+                                int W, int C, int k, int stride, int Ho, int Wo) {
+  const int cg = C / 8;
+  const int64_t total = (int64_t)n * Ho * Wo * cg;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int g = (int)(i % cg);
+  int64_t p = i / cg;
+  const int wo = (int)(p % Wo); p /= Wo;
+  const int ho = (int)(p % Ho);
+  const int img = (int)(p / Ho);
+  const int kh = k ? k : H, kw = k ? k : W;
+  const int h0 = k ? ho * stride : 0, w0 = k ? wo * stride : 0;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int u = 0; u < kh; ++u)
+    for (int v = 0; v < kw; ++v) {
+      const uint4 q = *reinterpret_cast<const uint4 *>(x + (((int64_t)img * H + h0 + u) * W + w0 + v) * C + g * 8);
+      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] += bf2f((uint16_t)(w4[e] & 0xffff));
+        acc[2 * e + 1] += bf2f((uint16_t)(w4[e] >> 16));
+      }
+    }
+  const float d = (float)(kh * kw);
+  uint32_t o[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = f2bf2(acc[2 * e] / d, acc[2 * e + 1] / d);
+  *reinterpret_cast<uint4 *>(y + i * 8) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 // ------------------------------------------------------------- transposes
 // [n, R, S] -> [n, S, R] through a 64 x 64 LDS tile (rows padded by one
 // element against bank conflicts); both global sides are coalesced.
@@ -359,8 +392,8 @@ __global__ void affine_kernel(const uint16_t *__restrict__ x, const float *__res
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int c = g * 8 + 2 * j;
-    float lo = bf2f((uint16_t)(w4[j] & 0xffff)) * scale[c] + shift[c];
-    float hi = bf2f((uint16_t)(w4[j] >> 16)) * scale[c + 1] + shift[c + 1];
+    float lo = __builtin_fmaf(bf2f((uint16_t)(w4[j] & 0xffff)), scale[c], shift[c]);
+    float hi = __builtin_fmaf(bf2f((uint16_t)(w4[j] >> 16)), scale[c + 1], shift[c + 1]);
     if (RELU) {
       lo = fmaxf(lo, 0.0f);
       hi = fmaxf(hi, 0.0f);
@@ -426,7 +459,10 @@ hipError_t launch_maxpool(bool bf16, const void *x, void *y, int n, int H, int W
 hipError_t launch_avgpool(bool bf16, const void *x, void *y, int n, int H, int W, int C, int k,
                           int stride, int Ho, int Wo, hipStream_t s) {
   const int64_t total = (int64_t)n * Ho * Wo * C;
-  if (bf16)
+  if (bf16 && C % 8 == 0 && (uintptr_t)x % 16 == 0 && (uintptr_t)y % 16 == 0)
+    hapi_launch(avgpool8_kernel, dim3(blocks_for(total / 8, 256)), dim3(256), 0, s, (const uint16_t *)x,
+                (uint16_t *)y, n, H, W, C, k, stride, Ho, Wo);
+  else if (bf16)
     hapi_launch(avgpool_kernel<uint16_t>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
                        (const uint16_t *)x, (uint16_t *)y, n, H, W, C, k, stride, Ho, Wo);
   else

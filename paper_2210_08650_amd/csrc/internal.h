@@ -83,7 +83,13 @@ struct ConvArgs {
   // LD_CAT only: second source [n, H2, W2, C2] NHWC, read at stride s2; K1 = % 64
   const void *x2;
   int H2, W2, C2, s2, K1;
+  // LD_GEMM only: row stride of x in elements (0: K), and a pre-activation
+  // applied to every element of x as it is read, x' = ReLU(x * pre_scale[k] +
+  // pre_shift[k]) rounded to bf16 (pre_scale null: none; K <= kPreMax).
+  int lda;
+  const float *pre_scale, *pre_shift;
 };
+constexpr int kPreMax = 1024;
 
 hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s);
 hipError_t launch_conv_f32(const ConvArgs &a, Loader ld, hipStream_t s);

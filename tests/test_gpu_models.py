@@ -318,3 +318,41 @@ def test_concurrent_requests_match_sequential(streams):
     torch.cuda.synchronize()
     assert not errors, errors
     assert torch.equal(out, seq)
+
+
+@pytest.mark.parametrize("cin,cout,hw", [(256, 128, (13, 11)), (128, 64, (7, 9)), (1024, 512, (7, 7))])
+def test_preact_conv_fused_equals_batchnorm_then_conv(cin, cout, hw):
+    """The pre-activation 1x1 convolution applies BN + ReLU to its operand as
+    it reads it; the result must equal, bit for bit, a separate batch-norm +
+    ReLU layer followed by the plain convolution (the same bf16 rounding of
+    the activated input, the same MFMA order)."""
+    shape = (cin,) + hw
+    man = [((cin,), "bn_gamma"), ((cin,), "bn_beta"), ((cin,), "bn_mean"), ((cin,), "bn_var"),
+           ((cout, cin, 1, 1), "he")]
+    ps = synth.params(96, man)
+    fused = Runner([PM.maxpool(1, 1), PM.preact_conv(cin, cout)], H.HAPI_BF16, ps, shape)
+    split = Runner([PM.maxpool(1, 1), PM.batchnorm(cin, relu=True),
+                    PM.conv(cin, cout, 1, relu=False)], H.HAPI_BF16, ps, shape)
+    x = synth.images(97, 3, cin, *hw)
+    xd, xv = images_for(H.HAPI_BF16, x)
+    a = fused.extract(xd, 2)
+    b = split.extract(xd, 3)
+    print(f"preact {cin}->{cout} at {hw}: max |a - b| {float((a.float() - b.float()).abs().max()):.3g}",
+          flush=True)
+    assert torch.equal(a, b)
+    om = OM.Model("preact", [OM.MaxPool(1, 1), OM.PreActConv(cin, cout)], shape)
+    assert rel_l2(a.float().cpu().numpy(), om.forward(ps, xv, 2)) <= 2e-2
+
+
+@pytest.mark.parametrize("c,hw", [(64, (14, 10)), (24, (15, 11)), (4, (6, 6))])
+def test_window_average_pooling_is_exact(c, hw):
+    """2 x 2 / 2 average pooling on eighths of small integers: every sum and
+    mean is exact in bf16, so the result equals the oracle's bit for bit
+    (16-byte path for channels % 8 == 0, element path otherwise)."""
+    shape = (c,) + hw
+    r = Runner([PM.avgpool(2, 2)], H.HAPI_BF16, [], shape)
+    x = synth.small_ints(98, (3,) + shape, -24, 24) / 8.0
+    xd, xv = images_for(H.HAPI_BF16, x)
+    got = r.extract(xd, 1).float().cpu().numpy()
+    om = OM.Model("pool", [OM.AvgPool(2, 2)], shape)
+    assert np.array_equal(got, om.forward([], xv, 1).astype(np.float32))
