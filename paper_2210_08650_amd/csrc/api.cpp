@@ -560,6 +560,17 @@ const Act &act_at(const Model &m, int start) {
 // images of one pixel or one channel.
 bool layout_free(const Act &a) { return a.tok || a.h * a.w == 1 || a.c == 1; }
 
+// A bottleneck with an identity shortcut whose 3 x 3 convolution the
+// row-streaming kernel runs (64 channels, stride 1) and whose expansion is
+// 64 -> 256: both run as one kernel.
+bool expand_fusable(const LayerPlan &lp) {
+  if (lp.L.kind != HAPI_BOTTLENECK || lp.has_sc || lp.convs.size() != 3 || lp.convs[2].fused) return false;
+  const ConvSpec &c2 = lp.convs[1], &c3 = lp.convs[2];
+  return c3.k == 1 && c3.stride == 1 && c3.pad == 0 && c3.cin == c2.cout &&
+         conv3x3_c64_supported(c2.cin, c2.cout, c2.k, c2.k, c2.stride, c2.pad, lp.in.w, c2.Kp, c2.cout, c2.cout) &&
+         conv3x3_c64_expand_supported(c3.cout, c3.K, c3.Kp, c3.cout, c3.cout);
+}
+
 // Runs layers start+1..split on nb images of `images` (the layer-`start`
 // tensor in the caller layout); writes the split output (caller layout) to
 // `out` unless it is null (profiling).
@@ -687,6 +698,23 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         const Act a1{width, lp.in.h, lp.in.w, false};
         const Act a2{width, lp.out.h, lp.out.w, false};
         HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
+        if (expand_fusable(lp)) {
+          // The 3 x 3 and the expanding 1 x 1 in one kernel, in place over the
+          // block input (each output element's residual is read by the lane
+          // that writes it, before it writes it).
+          const ConvSpec &c2 = lp.convs[1], &c3 = lp.convs[2];
+          const double px = (double)nb * a2.h * a2.w;
+          const double flops = 2.0 * px * (c2.cout * (double)c2.K + c3.cout * (double)c3.K);
+          const double bytes = (double)m.esz * (px * (c2.cin + 2.0 * c3.cout) + (double)c2.cout * c2.Kp +
+                                                (double)c3.cout * c3.Kp);
+          HIP_TRY(timed(c.s, F_CONV_BF16, flops, bytes, [&] {
+            return launch_conv3x3_c64(c.slot[A], c.pk + c2.pk_w, c2.Kp, reinterpret_cast<const float *>(c.pk + c2.pk_b),
+                                      cur, c3.cout, c.slot[cur_slot], c3.cout, nb, a1.h, a1.w, true, cu_count(), c.s,
+                                      c.pk + c3.pk_w, c3.Kp, reinterpret_cast<const float *>(c.pk + c3.pk_b));
+          }));
+          cur = c.slot[cur_slot];
+          break;
+        }
         HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], a1, nb, c.slot[B], nullptr, true, false, false));
         if (lp.convs[2].fused) {  // c3 and the projection shortcut in one GEMM, into the free slot
           HIP_TRY(run_conv(c, lp.convs[2], c.slot[B], a2, nb, c.slot[A], nullptr, true, false, false, 0,

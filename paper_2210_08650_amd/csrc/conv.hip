@@ -644,7 +644,9 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     if (m >= a.M) break;
     const float4 p = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8);
     const float4 q = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8 + 4);
-    float v[8] = {p.x, p.y, p.z, p.w, q.x, q.y, q.z, q.w};
+    // bias, then the residual: the order of every epilogue in the library
+    float v[8] = {p.x + bias[0], p.y + bias[1], p.z + bias[2], p.w + bias[3],
+                  q.x + bias[4], q.y + bias[5], q.z + bias[6], q.w + bias[7]};
     if (a.res) {
       const uint4 rv = rpre[EPI ? 0 : k];
       const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
@@ -657,8 +659,8 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
     uint32_t o[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float lo = epilogue_act(v[2 * e] + bias[2 * e], a.relu, a.gelu);
-      const float hi = epilogue_act(v[2 * e + 1] + bias[2 * e + 1], a.relu, a.gelu);
+      const float lo = epilogue_act(v[2 * e], a.relu, a.gelu);
+      const float hi = epilogue_act(v[2 * e + 1], a.relu, a.gelu);
       o[e] = f2bf2(lo, hi);
     }
     *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
@@ -973,7 +975,9 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
     if (m >= a.M) break;
     const float4 p = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8);
     const float4 q = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8 + 4);
-    float v[8] = {p.x, p.y, p.z, p.w, q.x, q.y, q.z, q.w};
+    // bias, then the residual: the order of every epilogue in the library
+    float v[8] = {p.x + bias[0], p.y + bias[1], p.z + bias[2], p.w + bias[3],
+                  q.x + bias[4], q.y + bias[5], q.z + bias[6], q.w + bias[7]};
     if (res) {
       const uint4 rv = rpre[EPI ? 0 : k];
       const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
@@ -986,8 +990,8 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
     uint32_t o[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float lo = epilogue_act(v[2 * e] + bias[2 * e], a.relu, a.gelu);
-      const float hi = epilogue_act(v[2 * e + 1] + bias[2 * e + 1], a.relu, a.gelu);
+      const float lo = epilogue_act(v[2 * e], a.relu, a.gelu);
+      const float hi = epilogue_act(v[2 * e + 1], a.relu, a.gelu);
       o[e] = f2bf2(lo, hi);
     }
     *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
@@ -1474,6 +1478,8 @@ hipError_t launch_short_ld(const ConvArgs &a, hipStream_t s) {
   return launch_short_cfg<BM, BN, WM, WN, 1, LD, MINB>(a, s);
 }
 
+}  // namespace
+
 // CUs of the current device (persistent grids use one workgroup per CU).
 int cu_count() {
   static int cached[64] = {0};
@@ -1486,6 +1492,8 @@ int cu_count() {
   }
   return cached[dev];
 }
+
+namespace {
 
 template <int BM, int BN, int WM, int WN, int PW, int STAGES, int LD, int KW, int EP>
 hipError_t launch_pws_cfg(const ConvArgs &a, hipStream_t s) {

@@ -60,12 +60,31 @@ struct Conv3Args {
   uint16_t *y;          // [n * H * W][ldc]
   int H, W, ldw, ldc, ldr, relu;
   int bands, band_rows;  // output rows [b * band_rows, ...) of each image per workgroup
+  // Expansion (EXPAND kernels): the 3 x 3 result, with bias and ReLU and
+  // rounded to bf16, is the 64-channel input of a 1 x 1 convolution to
+  // kExpand channels (packed [kExpand][ldw3]) with bias3, the residual res
+  // and ReLU; y and res then have kExpand channels per pixel.
+  const uint16_t *w3;
+  const float *bias3;
+  int ldw3;
 };
 
+constexpr int kExpand = 256;             // output channels of the expansion
+constexpr int kW3Pitch = kC + 8;         // bf16 pitch of an expansion weight row in LDS
+
+// EXPAND = false: the 3 x 3 convolution alone, input rows double-buffered in
+// a ring of 10 (a step reads 6 while the next 4 are stored).
+// EXPAND = true: the expansion weights take the LDS of four ring rows; the
+// ring holds the 6 rows a step reads, and the next step's rows replace the 4
+// oldest after a barrier, while the expansion runs.
+template <bool EXPAND>
 __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
+  constexpr int kRing = EXPAND ? 6 : kRows;
   __shared__ __attribute__((aligned(16))) uint16_t wts[kC * kWPitch];
-  __shared__ __attribute__((aligned(16))) uint16_t ring[kRows * kPix * kC];
-  __shared__ float bias_s[kC];
+  __shared__ __attribute__((aligned(16))) uint16_t ring[kRing * kPix * kC];
+  __shared__ __attribute__((aligned(16))) uint16_t w3s[EXPAND ? kExpand * kW3Pitch : 8];
+  __shared__ __attribute__((aligned(16))) float bias_s[kC];
+  __shared__ __attribute__((aligned(16))) float bias3_s[EXPAND ? kExpand : 4];
 
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -75,7 +94,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
   const int r1 = min(a.H, r0 + a.band_rows);
   const int64_t img_px = (int64_t)img * a.H * a.W;
 
-  // Input row h (-1 .. H) lives in ring slot (h + 1) % kRows; outside the
+  // Input row h (-1 .. H) lives in ring slot (h + 1) % kRing; outside the
   // image and in the padding columns it is zero.  Item it moves 16 bytes.
   // Branch-free: a chunk outside the image reads the image's first pixel and
   // is zeroed when stored, so the loads of a whole row set stay in flight.
@@ -91,19 +110,27 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
   constexpr int kPer = (kRowChunks + kThreads - 1) / kThreads;  // chunks per thread per row
   auto store_row = [&](int h, int it, const uint4 &v) {
     const int p = it >> 3, c = it & 7;
-    *reinterpret_cast<uint4 *>(ring + ring_off((h + 1) % kRows, p, c)) = v;
+    *reinterpret_cast<uint4 *>(ring + ring_off((h + 1) % kRing, p, c)) = v;
   };
 
   // Prologue: every load (weights and the first six input rows) is issued
   // before any store, so their latencies overlap.
   {
     constexpr int kWPer = kC * (kK / 8) / kThreads;  // chunks of 16 bytes
-    uint4 wv[kWPer];
+    constexpr int kW3Per = EXPAND ? kExpand * (kC / 8) / kThreads : 1;
+    uint4 wv[kWPer], w3v[kW3Per];
     uint4 iv[6][kPer];
 #pragma unroll
     for (int e = 0; e < kWPer; ++e) {
       const int i = t + e * kThreads, n = i / (kK / 8), k8 = i - n * (kK / 8);
       wv[e] = *reinterpret_cast<const uint4 *>(a.w + (int64_t)n * a.ldw + k8 * 8);
+    }
+    if constexpr (EXPAND) {
+#pragma unroll
+      for (int e = 0; e < kW3Per; ++e) {
+        const int i = t + e * kThreads, n = i / (kC / 8), k8 = i - n * (kC / 8);
+        w3v[e] = *reinterpret_cast<const uint4 *>(a.w3 + (int64_t)n * a.ldw3 + k8 * 8);
+      }
     }
 #pragma unroll
     for (int q = 0; q < 6; ++q)
@@ -114,6 +141,13 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
       const int i = t + e * kThreads, n = i / (kK / 8), k8 = i - n * (kK / 8);
       *reinterpret_cast<uint4 *>(wts + n * kWPitch + k8 * 8) = wv[e];
     }
+    if constexpr (EXPAND) {
+#pragma unroll
+      for (int e = 0; e < kW3Per; ++e) {
+        const int i = t + e * kThreads, n = i / (kC / 8), k8 = i - n * (kC / 8);
+        *reinterpret_cast<uint4 *>(w3s + n * kW3Pitch + k8 * 8) = w3v[e];
+      }
+    }
 #pragma unroll
     for (int q = 0; q < 6; ++q)
 #pragma unroll
@@ -121,6 +155,9 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
         if (t + e * kThreads < kRowChunks) store_row(r0 - 1 + q, t + e * kThreads, iv[q][e]);
   }
   if (t < kC) bias_s[t] = a.bias ? a.bias[t] : 0.0f;
+  if constexpr (EXPAND) {
+    if (t < kExpand) bias3_s[t] = a.bias3 ? a.bias3[t] : 0.0f;
+  }
   __syncthreads();
 
   // Fragment offsets: A (weights) row n = 32 j + lane % 32 at k = 16 s + 8 lh;
@@ -142,6 +179,24 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
     }
     const int row = ho + (wave & (kStepRows - 1));  // this wave's output row
     const int pi = wave / kStepRows;                 // and its 32-pixel half
+    const int px = 32 * pi + lrow;
+    const int64_t m = img_px + (int64_t)row * a.W + px;
+    const bool live = row < r1 && px < a.W;
+    // EXPAND: the residual of this lane's outputs, loaded now so that its
+    // latency hides behind the 3 x 3 MFMAs.  Part (h, jn, q) holds channels
+    // 128 h + 32 jn + 16 q + 8 lh .. + 8 of pixel px.
+    uint4 rr[EXPAND ? 2 : 1][EXPAND ? 4 : 1][2];
+    if constexpr (EXPAND) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int jn = 0; jn < 4; ++jn)
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+            rr[h][jn][q] = (live && a.res)
+                               ? *reinterpret_cast<const uint4 *>(a.res + m * a.ldr + 128 * h + 32 * jn + 16 * q + 8 * lh)
+                               : make_uint4(0u, 0u, 0u, 0u);
+    }
     f32x16_t acc[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j)
@@ -154,13 +209,13 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
       constexpr int kSteps = 36, kAhead = 3, kSlots = kAhead + 1;
       int slot_base[3];
 #pragma unroll
-      for (int kh = 0; kh < 3; ++kh) slot_base[kh] = ((row + kh) % kRows) * kPix * kC;
+      for (int kh = 0; kh < 3; ++kh) slot_base[kh] = ((row + kh) % kRing) * kPix * kC;
       bf16x8_t fw0[kSlots], fw1[kSlots], fx[kSlots];
       auto read_step = [&](int st, int sl) {
         const int kh = st / 12, kw = (st / 4) % 3, cs = st % 4;
         fw0[sl] = *reinterpret_cast<const bf16x8_t *>(wts + aoff0 + 16 * st);
         fw1[sl] = *reinterpret_cast<const bf16x8_t *>(wts + aoff1 + 16 * st);
-        const int p = 32 * pi + lrow + kw;
+        const int p = px + kw;
         fx[sl] = *reinterpret_cast<const bf16x8_t *>(ring + slot_base[kh] + p * kC + (((2 * cs + lh) ^ ((p >> 1) & 7)) << 3));
       };
       static_for<kAhead>([&](auto sc) { read_step(decltype(sc)::value, decltype(sc)::value); });
@@ -171,39 +226,42 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
         acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw1[sl], fx[sl], acc[1], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       });
-      // acc[j][4 g + e] = channel 32 j + 8 g + 4 lh + e of pixel 32 pi + lane % 32.
-      // After the half-wave exchange of part q, a lane owns channels
-      // 32 j + 16 q + 8 lh .. + 8 of that pixel.
-      {
-        const int px = 32 * pi + lrow;
-        const int64_t m = img_px + (int64_t)row * a.W + px;
+    }
+    // acc[j][4 g + e] = channel 32 j + 8 g + 4 lh + e of pixel px.  After the
+    // half-wave exchange of part q, a lane owns channels 32 j + 16 q + 8 lh
+    // .. + 8 of that pixel, with bias added.
+    auto finish8 = [&](const f32x16_t &c, int q, const float *bsrc, float v[8]) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(c[8 * q + e]),
+                                                         __float_as_uint(c[8 * q + 4 + e]), false, false);
+        v[e] = __uint_as_float(sw[0]);
+        v[4 + e] = __uint_as_float(sw[1]);
+      }
+      const float4 b0 = *reinterpret_cast<const float4 *>(bsrc);
+      const float4 b1 = *reinterpret_cast<const float4 *>(bsrc + 4);
+      v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+      v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+    };
+    auto add_res = [&](const uint4 &rv, float v[8]) {
+      const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] += __uint_as_float(w4[e] << 16);
+        v[2 * e + 1] += __uint_as_float(w4[e] & 0xffff0000u);
+      }
+    };
+    if constexpr (!EXPAND) {
+      if (row < r1) {
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
           for (int q = 0; q < 2; ++q) {
-            float v[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[j][8 * q + e]),
-                                                               __float_as_uint(acc[j][8 * q + 4 + e]), false, false);
-              v[e] = __uint_as_float(sw[0]);
-              v[4 + e] = __uint_as_float(sw[1]);
-            }
             const int n = 32 * j + 16 * q + 8 * lh;
-            const float4 b0 = *reinterpret_cast<const float4 *>(bias_s + n);
-            const float4 b1 = *reinterpret_cast<const float4 *>(bias_s + n + 4);
-            v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
-            v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+            float v[8];
+            finish8(acc[j], q, bias_s + n, v);
             if (px < a.W) {
-              if (a.res) {
-                const uint4 rv = *reinterpret_cast<const uint4 *>(a.res + m * a.ldr + n);
-                const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  v[2 * e] += __uint_as_float(w4[e] << 16);
-                  v[2 * e + 1] += __uint_as_float(w4[e] & 0xffff0000u);
-                }
-              }
+              if (a.res) add_res(*reinterpret_cast<const uint4 *>(a.res + m * a.ldr + n), v);
               uint32_t o[4];
 #pragma unroll
               for (int e = 0; e < 4; ++e)
@@ -212,15 +270,76 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
             }
           }
       }
-    }
-    if (more) {
+      if (more) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-          const int it = t + e * kThreads;
-          if (it < kRowChunks) store_row(ho + 5 + q, it, pre[q][e]);
+          for (int e = 0; e < kPer; ++e) {
+            const int it = t + e * kThreads;
+            if (it < kRowChunks) store_row(ho + 5 + q, it, pre[q][e]);
+          }
+      }
+    } else {
+      // Every wave has read the ring rows the next step's rows replace.
+      __syncthreads();
+      if (more) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < kPer; ++e) {
+            const int it = t + e * kThreads;
+            if (it < kRowChunks) store_row(ho + 5 + q, it, pre[q][e]);
+          }
+      }
+      if (row < r1) {
+        // The 3 x 3 result, rounded once, is the expansion's B operand: k-step
+        // s = 2 j + q covers channels 16 s .. 16 s + 15, of which this lane
+        // holds 16 s + 8 lh .. + 8 of pixel px.
+        bf16x8_t xb[4];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            float v[8];
+            finish8(acc[j], q, bias_s + 32 * j + 16 * q + 8 * lh, v);
+            uint32_t o[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              o[e] = a.relu ? f2bf2(fmaxf(v[2 * e], 0.0f), fmaxf(v[2 * e + 1], 0.0f)) : f2bf2(v[2 * e], v[2 * e + 1]);
+            xb[2 * j + q] = __builtin_bit_cast(bf16x8_t, make_uint4(o[0], o[1], o[2], o[3]));
+          }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          f32x16_t e3[4];
+#pragma unroll
+          for (int jn = 0; jn < 4; ++jn)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) e3[jn][e] = 0.0f;
+#pragma unroll
+          for (int s3 = 0; s3 < 4; ++s3)
+#pragma unroll
+            for (int jn = 0; jn < 4; ++jn) {
+              const bf16x8_t wf =
+                  *reinterpret_cast<const bf16x8_t *>(w3s + (128 * h + 32 * jn + lrow) * kW3Pitch + 16 * s3 + 8 * lh);
+              e3[jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xb[s3], e3[jn], 0, 0, 0);
+            }
+#pragma unroll
+          for (int jn = 0; jn < 4; ++jn)
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+              const int n = 128 * h + 32 * jn + 16 * q + 8 * lh;
+              float v[8];
+              finish8(e3[jn], q, bias3_s + n, v);
+              if (px < a.W) {
+                add_res(rr[h][jn][q], v);
+                uint32_t o[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = f2bf2(fmaxf(v[2 * e], 0.0f), fmaxf(v[2 * e + 1], 0.0f));
+                *reinterpret_cast<uint4 *>(y + m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+              }
+            }
         }
+      }
     }
     __syncthreads();
   }
@@ -233,8 +352,13 @@ bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, in
          Kp == kK && ldc % 8 == 0 && ldr % 8 == 0;
 }
 
+bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr) {
+  return N3 == kExpand && K3 == kC && Kp3 == kC && ldc % 8 == 0 && ldr % 8 == 0;
+}
+
 hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float *bias, const void *res, int ldr,
-                              void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s) {
+                              void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s,
+                              const void *w3, int ldw3, const float *bias3) {
   // Enough workgroups to fill the CUs: split images into bands of rows.
   int bands = (cus + n - 1) / n;
   bands = bands < 1 ? 1 : bands;
@@ -245,8 +369,11 @@ hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float
   bands = (H + band_rows - 1) / band_rows;
   Conv3Args a{static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(w), bias,
               static_cast<const uint16_t *>(res), static_cast<uint16_t *>(y), H, W, ldw, ldc, ldr, relu ? 1 : 0,
-              bands, band_rows};
-  hapi_launch(conv3x3_c64_kernel, dim3(n * bands), dim3(kThreads), 0, s, a);
+              bands, band_rows, static_cast<const uint16_t *>(w3), bias3, ldw3};
+  if (w3)
+    hapi_launch(conv3x3_c64_kernel<true>, dim3(n * bands), dim3(kThreads), 0, s, a);
+  else
+    hapi_launch(conv3x3_c64_kernel<false>, dim3(n * bands), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -136,8 +136,16 @@ constexpr int kS2DChannels = 16;
 // streamed once.  k = (kh, kw, c), packed [64][ldw]; optional residual;
 // cus = CUs to fill.
 bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, int W, int Kp, int ldc, int ldr);
+// With w3 (packed [256][ldw3], K = 64) the ReLU'd, bf16-rounded result is
+// expanded in the same kernel by a 1 x 1 convolution to 256 channels with
+// bias3, the residual res [.][ldr] and ReLU, into y [.][ldc] (a bottleneck's
+// last two convolutions); see conv3x3_c64_expand_supported.
 hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float *bias, const void *res, int ldr,
-                              void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s);
+                              void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s,
+                              const void *w3 = nullptr, int ldw3 = 0, const float *bias3 = nullptr);
+bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr);
+// Compute units of the current device.
+int cu_count();
 bool stem_pool_supported(int C, int H, int W, int cout, int Ho, int Wo, int Hp, int Wp);
 hipError_t launch_stem_pool_bf16(const void *x, const void *w, int ldw, const float *bias, void *y, int n, int C,
                                  int H, int W, int Ho, int Wo, int Hp, int Wp, hipStream_t s);

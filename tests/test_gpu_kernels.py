@@ -118,3 +118,40 @@ def test_identity_kernel_conv_is_exact_on_random_values():
         r2 = Runner([PM.maxpool(1, 1), PM.conv(C, C, 3, 2, 1, bias=True, relu=False)], dtype,
                     [w, np.zeros(C, np.float32)], (C, 11, 11))
         assert np.array_equal(r2.extract_np(xd, 2), xv[:, :, ::2, ::2])
+
+
+@pytest.mark.parametrize("hw,batch", [(20, 3), (56, 2), (9, 2)])
+def test_fused_bottleneck_block_exact(hw, batch):
+    """A stage-1 bottleneck with an identity shortcut runs its 3x3 and its
+    expanding 1x1 convolution as one kernel (the 3x3 result stays on chip,
+    rounded once to bf16, as the expansion's operand).  With small-integer
+    data and batch-norm scales of exactly one, every sum is exact and the
+    only roundings are the three bf16 roundings of the block, which the
+    reference applies at the same points: the output must match bit for bit."""
+    cin, w = 256, 64
+    var = np.float32(1.0) - np.float32(1e-5)   # var + 1e-5 == 1 in float32
+    assert var + np.float32(1e-5) == np.float32(1.0)
+
+    def bn(seed, c):
+        return [np.ones(c, np.float32), synth.small_ints(seed, (c,), -2, 2),
+                np.zeros(c, np.float32), np.full(c, var, np.float32)]
+    w1 = synth.small_ints(300, (w, cin, 1, 1), -1, 1)
+    w2 = synth.small_ints(301, (w, w, 3, 3), -1, 1)
+    w3 = synth.small_ints(302, (4 * w, w, 1, 1), -1, 1)
+    b1, b2, b3 = bn(303, w), bn(304, w), bn(305, 4 * w)
+    params = [w1] + b1 + [w2] + b2 + [w3] + b3
+    layers = [PM.maxpool(1, 1), dict(kind=H.HAPI_BOTTLENECK, cin=cin, width=w, cout=4 * w, stride=1)]
+    r = Runner(layers, H.HAPI_BF16, params, (cin, hw, hw))
+    x = synth.small_ints(306, (batch, cin, hw, hw), -2, 2)
+    xd, xv = images_for(H.HAPI_BF16, x)
+    H.hapi_stats_enable(True)
+    got = r.extract_np(xd, 2)
+    st = {s["name"]: s for s in H.hapi_stats_collect()}
+    H.hapi_stats_enable(False)
+    assert st["conv_bf16"]["launches"] == 2     # c1, then 3x3 + expansion together
+    h1 = bf16_round(np.maximum(L.conv2d(xv, w1, b1[1], 1, 0), 0))
+    h2 = bf16_round(np.maximum(L.conv2d(h1, w2, b2[1], 1, 1), 0))
+    ref = bf16_round(np.maximum(L.conv2d(h2, w3, b3[1], 1, 0) + xv, 0))
+    print(f"fused bottleneck {hw}x{hw} batch {batch}: max |h2| {np.abs(h2).max():.0f}, "
+          f"max |y| {np.abs(ref).max():.0f}", flush=True)
+    assert np.array_equal(got, ref), np.abs(got - ref).max()
