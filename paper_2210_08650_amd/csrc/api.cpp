@@ -465,6 +465,7 @@ struct Ctx {
   const uint8_t *pk;
   uint8_t *slot[3];
   std::function<void(int, bool)> on_layer;  // (layer index, begin) for profiling
+  int cus;  // workgroups of persistent kernels
 };
 
 // Per-channel scale and shift (an inference batch-norm) that a 1 x 1
@@ -479,6 +480,7 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
                     void *y, const void *res, bool relu, bool gelu, bool nchw_input, int ldc = 0,
                     const void *x2 = nullptr, const Act *in2 = nullptr, PreAct pre = PreAct{}) {
   ConvArgs a{};
+  a.cus = c.cus;
   a.pre_scale = pre.scale;
   a.pre_shift = pre.shift;
   a.lda = pre.lda;
@@ -709,7 +711,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
                                                 (double)c3.cout * c3.Kp);
           HIP_TRY(timed(c.s, F_CONV_BF16, flops, bytes, [&] {
             return launch_conv3x3_c64(c.slot[A], c.pk + c2.pk_w, c2.Kp, reinterpret_cast<const float *>(c.pk + c2.pk_b),
-                                      cur, c3.cout, c.slot[cur_slot], c3.cout, nb, a1.h, a1.w, true, cu_count(), c.s,
+                                      cur, c3.cout, c.slot[cur_slot], c3.cout, nb, a1.h, a1.w, true, c.cus, c.s,
                                       c.pk + c3.pk_w, c3.Kp, reinterpret_cast<const float *>(c.pk + c3.pk_b));
           }));
           cur = c.slot[cur_slot];
@@ -919,10 +921,13 @@ int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, con
   }
   std::vector<Ctx> c;
   c.reserve(lanes);
+  // Persistent kernels of every lane size their grid to the whole device:
+  // halving it per lane was measured slower (ResNet-50 b256: 69.5k -> 66k img/s).
+  const int cus = cu_count();
   for (int i = 0; i < lanes; ++i) {
     uint8_t *w0 = ws + (int64_t)i * 3 * sb;
     c.push_back(Ctx{m, i ? L->aux[i - 1] : s, static_cast<const uint8_t *>(weights),
-                    {w0, w0 + sb, w0 + 2 * sb}, on_layer});
+                    {w0, w0 + sb, w0 + 2 * sb}, on_layer, cus});
   }
   const int64_t in_bytes = act_at(m, start).elems() * m.esz;
   const int64_t out_bytes = m.layers[split - 1].out.elems() * m.esz;

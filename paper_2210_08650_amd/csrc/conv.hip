@@ -1498,7 +1498,8 @@ namespace {
 template <int BM, int BN, int WM, int WN, int PW, int STAGES, int LD, int KW, int EP>
 hipError_t launch_pws_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  const int grid = tiles < cu_count() ? tiles : cu_count();
+  const int cus = a.cus > 0 ? a.cus : cu_count();
+  const int grid = tiles < cus ? tiles : cus;
   hapi_launch((conv_bf16_pws_kernel<BM, BN, WM, WN, PW, STAGES, LD, KW, EP>), dim3(grid),
                      dim3((WM * WN + PW) * 64), 0, s, a);
   return hipGetLastError();
@@ -2058,7 +2059,7 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
       if (!a.gelu && a.Ho == a.H && a.Wo == a.W && forced_cfg() < 0 &&
           conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
         return launch_conv3x3_c64(a.x, a.w, a.Kp, a.bias, a.res, a.ldr, a.y, a.ldc, a.n_img, a.H, a.W, a.relu != 0,
-                                  cu_count(), s);
+                                  a.cus > 0 ? a.cus : cu_count(), s);
       return (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) ? launch_pipe_ld<LD_NHWC>(a, s)
                                                                  : launch_bf16_ld<LD_NHWC>(a, s);
     case LD_GEMM:

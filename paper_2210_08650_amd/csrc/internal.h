@@ -88,6 +88,8 @@ struct ConvArgs {
   // pre_shift[k]) rounded to bf16 (pre_scale null: none; K <= kPreMax).
   int lda;
   const float *pre_scale, *pre_shift;
+  // Workgroups of the persistent kernels (0: one per CU).
+  int cus;
 };
 constexpr int kPreMax = 1024;
 
