@@ -40,9 +40,25 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
 __device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float((uint32_t)u << 16); }
 
 
+// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26:
+// erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2), t = 1 / (1 + p x)
+// for x >= 0 (odd extension), absolute error <= 1.5e-7: branch-free, one
+// reciprocal and one exponential, against a piecewise library erf.
+__device__ __forceinline__ float erf_as(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
+  float q = fmaf(t, 1.061405429f, -1.453152027f);
+  q = fmaf(t, q, 1.421413741f);
+  q = fmaf(t, q, -0.284496736f);
+  q = fmaf(t, q, 0.254829592f);
+  const float y = fmaf(-t * q, __builtin_amdgcn_exp2f(-ax * ax * 1.4426950408889634f), 1.0f);
+  return copysignf(y, x);
+}
+
+// GELU is the exact (erf) form: v * Phi(v) = 0.5 v (1 + erf(v / sqrt 2)).
 __device__ __forceinline__ float epilogue_act(float v, int relu, int gelu) {
   if (relu) v = fmaxf(v, 0.0f);
-  if (gelu) v = 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+  if (gelu) v = 0.5f * v * (1.0f + erf_as(v * 0.70710678118654752f));
   return v;
 }
 
