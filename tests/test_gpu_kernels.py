@@ -56,6 +56,9 @@ BF16_CASES = [
     (True, 64, 64, 3, 1, 1, 56, 2),      # row-streaming 3x3, 64 -> 64 (ResNet stage 1)
     (True, 64, 64, 3, 1, 1, 17, 3),      # row-streaming 3x3, ragged rows and bands
     (True, 64, 64, 3, 1, 1, 64, 1),      # row-streaming 3x3 at its widest row
+    (True, 128, 32, 3, 1, 1, 15, 3),     # 32 output channels, few rows: 128 x 64 tiles
+    (True, 128, 32, 3, 1, 1, 256, 2),    # 32 output channels, M = 131072: 256 x 32 tiles
+    (True, 128, 24, 3, 1, 1, 256, 2),    # 24 output channels in a 32-column tile
 ]
 
 
