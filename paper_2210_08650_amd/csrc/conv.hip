@@ -744,7 +744,7 @@ struct WsPlan {
       const int n = mm / hw, rem = mm - n * hw;
       const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
       if (LD == LD_GEMM) {
-        va[0][i] = valid ? (unsigned)(((int64_t)m * a.K + kc8) * 2) : kOob;
+        va[0][i] = valid ? (unsigned)(((int64_t)m * (a.lda ? a.lda : a.K) + kc8) * 2) : kOob;
       } else if (LD == LD_S2D) {  // k-tile du adds du * W * C (scalar)
         va[0][i] = valid ? (unsigned)(((((int64_t)n * a.H + ho) * a.W + wo) * a.C + kc8) * 2) : kOob;
       } else if (LD == LD_NCHW_PATCH) {  // kw == 16: k-tile = 4 kernel rows of one channel
@@ -771,7 +771,7 @@ struct WsPlan {
   }
 };
 
-template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI>
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI, bool PRE = false>
 __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   constexpr int CW = WM * WN;                      // consumer waves (= producer waves)
   constexpr int NT = 2 * CW * 64;
@@ -785,6 +785,7 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   static_assert(STAGES >= 2 && STAGES <= 4 && (STAGES - 2) * NQ < 64, "stages");
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[SM::kBytes];
   uint16_t *smem = reinterpret_cast<uint16_t *>(smem_raw);
+  __shared__ __attribute__((aligned(16))) float pre_s[PRE ? 2 * kPreMax : 4];
 
   const int tiles_n = (a.N + BN - 1) / BN;
   const int tile = xcd_remap(blockIdx.x, gridDim.x);
@@ -793,6 +794,16 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // uniform: keeps LDS addresses scalar
   const bool producer = wave >= CW;
   const int nk = a.Kp / BK;
+  if constexpr (PRE) {
+    // Zero beyond K: the columns of the last k-tile past K (which the loader
+    // reads from the next channels of the row) become exact zeros, whatever
+    // they hold (ReLU maps NaN to 0).
+    for (int c = t; c < a.Kp; c += NT) {
+      pre_s[c] = c < a.K ? a.pre_scale[c] : 0.0f;
+      pre_s[kPreMax + c] = c < a.K ? a.pre_shift[c] : 0.0f;
+    }
+    __syncthreads();
+  }
 
   const int wm = (wave % CW) / WN, wn = (wave % CW) % WN;
   const int lrow = lane & 31, lh = lane >> 5;
@@ -894,22 +905,30 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
     for (int j = 0; j < TN; ++j) boff[j] = BM * BK + (wn * TN * 32 + j * 32 + lrow) * BK;
     const int sw = (lrow >> 1) & 7;
     bf16x8_t af[2][TM], bfr[2][TN];
-    auto read_frags = [&](const uint16_t *S, int ks, int buf) {
+    auto read_frags = [&](const uint16_t *S, int ks, int buf, int kt) {
       const int ch = ((2 * ks + lh) ^ sw) * 8;
 #pragma unroll
       for (int i = 0; i < TM; ++i) af[buf][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
 #pragma unroll
       for (int j = 0; j < TN; ++j) bfr[buf][j] = *reinterpret_cast<const bf16x8_t *>(S + boff[j] + ch);
+      if constexpr (PRE) {
+        const float *ps = pre_s + kt * BK + (2 * ks + lh) * 8;
+        const float4 s0 = *reinterpret_cast<const float4 *>(ps), s1 = *reinterpret_cast<const float4 *>(ps + 4);
+        const float4 h0 = *reinterpret_cast<const float4 *>(ps + kPreMax);
+        const float4 h1 = *reinterpret_cast<const float4 *>(ps + kPreMax + 4);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[buf][i] = preact8(af[buf][i], s0, s1, h0, h1);
+      }
     };
     for (int kt = 0; kt < nk; ++kt) {
       __builtin_amdgcn_s_barrier();
       const uint16_t *S = smem + (kt % STAGES) * SM::kStage;
-      read_frags(S, 0, 0);
+      read_frags(S, 0, 0, kt);
       __builtin_amdgcn_sched_barrier(0);
       static_for<KS>([&](auto ksc) {
         constexpr int ks = decltype(ksc)::value;
         constexpr int cur = ks & 1;
-        if constexpr (ks + 1 < KS) read_frags(S, ks + 1, cur ^ 1);
+        if constexpr (ks + 1 < KS) read_frags(S, ks + 1, cur ^ 1, kt);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -1019,16 +1038,16 @@ template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI>
 __global__ __launch_bounds__(2 * WM * WN * 64) void conv_bf16_ws_kernel(ConvArgs a) {
   conv_bf16_ws_body<BM, BN, WM, WN, STAGES, LD, KW, EPI>(a);
 }
-template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI>
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI, bool PRE = false>
 __global__ __launch_bounds__(2 * WM * WN * 64, 2) void conv_bf16_ws2_kernel(ConvArgs a) {
-  conv_bf16_ws_body<BM, BN, WM, WN, STAGES, LD, KW, EPI>(a);
+  conv_bf16_ws_body<BM, BN, WM, WN, STAGES, LD, KW, EPI, PRE>(a);
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 0, int MINB = 1>
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 0, int MINB = 1, bool PRE = false>
 hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if constexpr (MINB >= 2)
-    hapi_launch((conv_bf16_ws2_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
+    hapi_launch((conv_bf16_ws2_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI, PRE>), dim3(tiles),
                        dim3(2 * WM * WN * 64), 0, s, a);
   else
     hapi_launch((conv_bf16_ws_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
@@ -2068,6 +2087,12 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
       return hipErrorInvalidValue;
     if (!a.pre_scale) return launch_pipe_cfg<128, 128, 2, 2, 2, LD_GEMM, 1, 0>(a, s);
     if (a.N <= 64) return launch_pipe_cfg<128, 64, 2, 2, 3, LD_GEMM, 1, 0, true>(a, s);
+    // Warp-specialised with the pre-activation: the ragged last k-tile reads
+    // the row's next channels (inside the row when lda >= Kp), which the
+    // zero scale and shift turn into zeros.
+    if (a.Kp >= 2 * BK && (a.lda ? a.lda : a.K) >= a.Kp &&
+        (int64_t)a.M * (a.lda ? a.lda : a.K) * 2 < ((int64_t)1 << 31))
+      return launch_ws_cfg<128, 128, 2, 2, 2, LD_GEMM, 1, 0, 2, true>(a, s);
     return launch_pipe_cfg<128, 128, 2, 2, 2, LD_GEMM, 1, 0, true>(a, s);
   }
   if (launch_stream(a, ld, s) == hipSuccess) return hipSuccess;
