@@ -20,7 +20,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 
 template <int TP>
-__global__ __launch_bounds__(256) void attention_kernel(const uint16_t *__restrict__ qkv,
+__global__ __launch_bounds__(256, 2) void attention_kernel(const uint16_t *__restrict__ qkv,
                                                         uint16_t *__restrict__ out, int T, int D,
                                                         int heads, float scale_log2) {
   constexpr int DH = kHeadDim;       // 64
@@ -77,6 +77,8 @@ __global__ __launch_bounds__(256) void attention_kernel(const uint16_t *__restri
         const bf16x8_t ka = *reinterpret_cast<const bf16x8_t *>(Ks + (32 * t + col) * KP + ks * 16 + hl * 8);
         s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s[t], 0, 0, 0);
       }
+      // one key tile's fragments live at a time (keeps two waves per SIMD)
+      __builtin_amdgcn_sched_barrier(0);
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -123,6 +125,7 @@ __global__ __launch_bounds__(256) void attention_kernel(const uint16_t *__restri
           const bf16x8_t va = *reinterpret_cast<const bf16x8_t *>(&pack);
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[db], 0, 0, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (q < T) {
