@@ -34,19 +34,36 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(const uint16_t *__res
   const int ld = 3 * D;
   const uint16_t *base = qkv + (int64_t)img * T * ld;
 
-  for (int idx = threadIdx.x; idx < TP * 8; idx += 256) {
-    const int s = idx >> 3, c = idx & 7;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (s < T) {
-      kv = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + D + h * DH + c * 8);
-      vv = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + 2 * D + h * DH + c * 8);
-    }
-    *reinterpret_cast<uint4 *>(Ks + s * KP + c * 8) = kv;
-    const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+  // Staging: thread t < TP owns 8 keys (8 (t / 8) ..) x 8 channels (8 (t % 8) ..):
+  // all 16 loads first, then the key rows as they are and the 8 x 8 value
+  // block transposed in registers, written as 8 rows of V^T with 16-byte stores.
+  static_assert(TP <= 256, "one 8 x 8 block per thread");
+  if (threadIdx.x < TP) {
+    const int kb = threadIdx.x >> 3, c = threadIdx.x & 7;
+    uint4 kv[8], vv[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      Vt[(c * 8 + 2 * j) * VP + s] = (uint16_t)(w4[j] & 0xffff);
-      Vt[(c * 8 + 2 * j + 1) * VP + s] = (uint16_t)(w4[j] >> 16);
+    for (int r = 0; r < 8; ++r) {
+      const int s = 8 * kb + r;
+      kv[r] = vv[r] = make_uint4(0, 0, 0, 0);
+      if (s < T) {
+        kv[r] = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + D + h * DH + c * 8);
+        vv[r] = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + 2 * D + h * DH + c * 8);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) *reinterpret_cast<uint4 *>(Ks + (8 * kb + r) * KP + c * 8) = kv[r];
+    auto half = [&](const uint4 &q, int e) -> uint32_t {
+      const uint32_t w = (e >> 1) == 0 ? q.x : (e >> 1) == 1 ? q.y : (e >> 1) == 2 ? q.z : q.w;
+      return (e & 1) ? (w >> 16) : (w & 0xffffu);
+    };
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint4 o;
+      o.x = half(vv[0], e) | (half(vv[1], e) << 16);
+      o.y = half(vv[2], e) | (half(vv[3], e) << 16);
+      o.z = half(vv[4], e) | (half(vv[5], e) << 16);
+      o.w = half(vv[6], e) | (half(vv[7], e) << 16);
+      *reinterpret_cast<uint4 *>(Vt + (c * 8 + e) * VP + 8 * kb) = o;
     }
   }
   __syncthreads();
@@ -80,23 +97,25 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(const uint16_t *__res
       // one key tile's fragments live at a time (keeps two waves per SIMD)
       __builtin_amdgcn_sched_barrier(0);
     }
+    // Only the last key tile can hold padding keys (TP is T rounded up to 32).
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = 32 * (NT - 1) + 8 * (r >> 2) + 4 * hl + (r & 3);
+      if (key >= T) s[NT - 1][r] = -INFINITY;
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
-        const float v = key < T ? s[t][r] : -INFINITY;
-        s[t][r] = v;
-        mx = fmaxf(mx, v);
-      }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     float sum = 0.0f;
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f((s[t][r] - mx) * scale_log2);
+        // arguments are <= 0: the hardware exp2 (v_exp_f32) is exact enough
+        const float p = __builtin_amdgcn_exp2f((s[t][r] - mx) * scale_log2);
         s[t][r] = p;
         sum += p;
       }
