@@ -67,6 +67,7 @@ struct ConvSpec {
   bool fused;
   int K1, cin2, stride2;
   int64_t raw_w2, raw_bn2;
+  int splits;  // fp32 CONV layers: reduction slices (see f32_splits); else 1
 };
 
 struct Extra {  // float32 parameters: copied verbatim (tokens, layernorm), or an
@@ -82,6 +83,7 @@ struct LayerPlan {
   std::vector<Extra> extras;
   bool has_sc = false;
   int64_t tmp_elems = 0;  // largest per-image tensor the layer reads or writes
+  int64_t part_elems = 0; // per-image fp32 partial sums of a split reduction
   int64_t pk_end = 0;     // packed-weight bytes of layers 1..this one
 };
 
@@ -119,6 +121,7 @@ int analyze(const hapi_model_desc *d, Model &m) {
     ConvSpec c{};
     c.cin = cin; c.cout = cout; c.k = k; c.stride = s; c.pad = p; c.bias = bias; c.bn = bn;
     c.s2d = s2d;
+    c.splits = 1;
     c.K = s2d ? ((k + 1) / 2) * ((k + 1) / 2) * kS2DChannels : cin * k * k;
     c.Kp = (c.K + kq - 1) / kq * kq;
     c.raw_w = raw; raw += (int64_t)cout * cin * k * k;
@@ -182,6 +185,13 @@ int analyze(const hapi_model_desc *d, Model &m) {
         add_conv(lp, L.cin, L.cout, L.k, L.stride, L.pad, L.has_bias != 0, L.has_bn != 0, s2d);
         lp.out = Act{L.cout, ho, wo, false};
         if (s2d) lp.tmp_elems = (int64_t)(ho + 3) * (wo + 3) * kS2DChannels;
+        if (!m.bf16 && L.cout % 4 == 0) {
+          // fp32: long reductions run as slices (the slice count depends on K
+          // only, so results do not depend on the batch or its partitions)
+          ConvSpec &cs = lp.convs.back();
+          cs.splits = f32_splits(cs.Kp);
+          if (cs.splits > 1) lp.part_elems = (int64_t)cs.splits * ho * wo * L.cout;
+        }
         if (first) m.first_reads_nchw = true;
         break;
       }
@@ -371,6 +381,12 @@ int inflight_for(const hapi_model_desc *d, int batch) {
   return (d->chunk == 0 && batch >= kAutoInflightBatch) ? 2 : 1;
 }
 
+int64_t max_part(const Model &m, int split) {
+  int64_t p = 0;
+  for (int i = 0; i < split; ++i) p = std::max(p, m.layers[i].part_elems);
+  return p;
+}
+
 int chunk_for(const hapi_model_desc *d, const Model &m, int batch) {
   const int lanes = inflight_for(d, batch);
   int c = d->chunk > 0 ? std::min(d->chunk, batch)
@@ -392,9 +408,15 @@ int lanes_for(const hapi_model_desc *d, int chunk, int batch) {
   return std::max(1, std::min(inflight_for(d, batch), (batch + chunk - 1) / chunk));
 }
 
-// Three activation slots per partition in flight (profiling runs one).
+// Bytes of one lane's fp32 partial-sum region.
+int64_t part_bytes(const Model &m, int split, int chunk) {
+  return align_up((int64_t)chunk * max_part(m, split) * 4);
+}
+
+// Three activation slots and the partial-sum region per partition in flight
+// (profiling runs one).
 int64_t workspace_for(const Model &m, int split, int chunk, bool profile, int batch, int lanes) {
-  int64_t b = split > 0 ? (profile ? 1 : lanes) * 3 * slot_bytes(m, split, chunk) : 0;
+  int64_t b = split > 0 ? (profile ? 1 : lanes) * (3 * slot_bytes(m, split, chunk) + part_bytes(m, split, chunk)) : 0;
   if (profile) b += align_up(m.packed_bytes) + align_up((int64_t)batch * m.input.elems() * m.esz);
   return b;
 }
@@ -411,9 +433,9 @@ LaunchEvents &launch_events() {
 namespace {
 
 enum Family { F_CONV_BF16, F_CONV_F32, F_ATTN, F_LN, F_MAXPOOL, F_AVGPOOL, F_TOKENS, F_LAYOUT,
-              F_COPY, F_AFFINE, F_COUNT };
+              F_COPY, F_AFFINE, F_SPLIT_SUM, F_COUNT };
 const char *kFamily[F_COUNT] = {"conv_bf16", "conv_f32", "attention", "layernorm", "maxpool",
-                                "avgpool", "tokens", "layout", "copy", "affine_relu"};
+                                "avgpool", "tokens", "layout", "copy", "affine_relu", "split_sum"};
 
 struct StatRec {
   int fam;
@@ -465,7 +487,8 @@ struct Ctx {
   const uint8_t *pk;
   uint8_t *slot[3];
   std::function<void(int, bool)> on_layer;  // (layer index, begin) for profiling
-  int cus;  // workgroups of persistent kernels
+  int cus;      // workgroups of persistent kernels
+  float *part;  // fp32 partial sums of split reductions
 };
 
 // Per-channel scale and shift (an inference batch-norm) that a 1 x 1
@@ -537,7 +560,13 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
                                           (double)a.N * a.K + (cs.fused ? (double)a.M * cs.cin2 : 0.0));
   if (c.m.bf16)
     return timed(c.s, F_CONV_BF16, flops, bytes, [&] { return launch_conv_bf16(a, ld, c.s); });
-  return timed(c.s, F_CONV_F32, flops, bytes, [&] { return launch_conv_f32(a, ld, c.s); });
+  a.splits = cs.splits;
+  a.part = c.part;
+  hipError_t r = timed(c.s, F_CONV_F32, flops, bytes, [&] { return launch_conv_f32(a, ld, c.s); });
+  if (r != hipSuccess || cs.splits <= 1) return r;
+  const double pbytes = 4.0 * a.M * a.N * (cs.splits + 1);
+  return timed(c.s, F_SPLIT_SUM, (double)a.M * a.N * cs.splits, pbytes,
+               [&] { return launch_f32_split_reduce(a, c.s); });
 }
 
 // A ResNet stem (7 x 7 stride-2 convolution with ReLU on space-to-depth
@@ -913,6 +942,7 @@ int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, con
               const std::function<void(int, bool)> &on_layer) {
   hipStream_t s = static_cast<hipStream_t>(d->stream);
   const int64_t sb = slot_bytes(m, split, chunk);
+  const int64_t lane_bytes = 3 * sb + part_bytes(m, split, chunk);
   Lanes *L = nullptr;
   if (lanes > 1) {
     if (int r = get_lanes(s, &L)) return r;
@@ -925,9 +955,9 @@ int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, con
   // halving it per lane was measured slower (ResNet-50 b256: 69.5k -> 66k img/s).
   const int cus = cu_count();
   for (int i = 0; i < lanes; ++i) {
-    uint8_t *w0 = ws + (int64_t)i * 3 * sb;
+    uint8_t *w0 = ws + (int64_t)i * lane_bytes;
     c.push_back(Ctx{m, i ? L->aux[i - 1] : s, static_cast<const uint8_t *>(weights),
-                    {w0, w0 + sb, w0 + 2 * sb}, on_layer, cus});
+                    {w0, w0 + sb, w0 + 2 * sb}, on_layer, cus, reinterpret_cast<float *>(w0 + 3 * sb)});
   }
   const int64_t in_bytes = act_at(m, start).elems() * m.esz;
   const int64_t out_bytes = m.layers[split - 1].out.elems() * m.esz;
@@ -1137,7 +1167,7 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
   if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(desc->stream);
   uint8_t *ws = static_cast<uint8_t *>(desc->workspace);
-  const int64_t slots = 3 * slot_bytes(m, n, chunk);
+  const int64_t slots = 3 * slot_bytes(m, n, chunk) + part_bytes(m, n, chunk);
   uint8_t *pk = ws + slots;
   uint8_t *img = pk + align_up(m.packed_bytes);
   // Synthetic model and inputs: small pseudo-random values in every parameter.

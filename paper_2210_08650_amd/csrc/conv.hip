@@ -1982,13 +1982,16 @@ __global__ __launch_bounds__(kThreads) void conv_f32_kernel(ConvArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = a.Kp / BKF;
-  load_tile(0);
+  // k-tiles [kt0, kt1): slice blockIdx.y of a split reduction, or all of them.
+  const int nk_all = a.Kp / BKF;
+  const int S = a.splits > 1 ? a.splits : 1;
+  const int kt0 = (int)((int64_t)nk_all * blockIdx.y / S), kt1 = (int)((int64_t)nk_all * (blockIdx.y + 1) / S);
+  load_tile(kt0);
   store_tile(0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load_tile(kt + 1);
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int cur = (kt - kt0) & 1;
+    if (kt + 1 < kt1) load_tile(kt + 1);
     const float *As = smem + cur * (BM + BN) * LDSF + (wm * TM * 32 + lrow) * LDSF + lk;
     const float *Bs = smem + cur * (BM + BN) * LDSF + BM * LDSF + (wn * TN * 32 + lrow) * LDSF + lk;
     // Lane half h feeds k = 8h + s at step s to both operands, so the 8 steps
@@ -2015,10 +2018,26 @@ __global__ __launch_bounds__(kThreads) void conv_f32_kernel(ConvArgs a) {
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][s], bv[j][s], acc[i][j], 0, 0, 0);
-    if (kt + 1 < nk) store_tile(cur ^ 1);
+    if (kt + 1 < kt1) store_tile(cur ^ 1);
     __syncthreads();
   }
 
+  if (S > 1) {  // partial sums of this slice; bias and activation come after the sum
+    float *part = a.part + (int64_t)blockIdx.y * a.M * a.N;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * TN * 32 + j * 32 + lrow;
+      if (n >= a.N) continue;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + wm * TM * 32 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (m < a.M) part[(int64_t)m * a.N + n] = acc[i][j][r];
+        }
+    }
+    return;
+  }
   float *y = static_cast<float *>(a.y);
   const float *res = static_cast<const float *>(a.res);
 #pragma unroll
@@ -2040,10 +2059,39 @@ __global__ __launch_bounds__(kThreads) void conv_f32_kernel(ConvArgs a) {
   }
 }
 
+// Sum of the slices in slice order, then bias, residual and activation (the
+// unsplit epilogue's order), 4 channels per thread.
+__global__ void f32_split_reduce_kernel(ConvArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int ng = a.N / 4;
+  if (i >= (int64_t)a.M * ng) return;
+  const int64_t m = i / ng;
+  const int n = (int)(i - m * ng) * 4;
+  const int64_t stride = (int64_t)a.M * a.N;
+  float4 v = *reinterpret_cast<const float4 *>(a.part + m * a.N + n);
+  for (int sl = 1; sl < a.splits; ++sl) {
+    const float4 p = *reinterpret_cast<const float4 *>(a.part + sl * stride + m * a.N + n);
+    v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+  }
+  float o[4] = {v.x, v.y, v.z, v.w};
+  const float *res = static_cast<const float *>(a.res);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float x = o[e] + (a.bias ? a.bias[n + e] : 0.0f);
+    if (res) x += res[m * a.ldr + n + e];
+    o[e] = epilogue_act(x, a.relu, a.gelu);
+  }
+  float *y = static_cast<float *>(a.y);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) y[m * a.ldc + n + e] = o[e];
+}
+
 template <int BM, int BN, int LD>
 hipError_t launch_f32_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hapi_launch((conv_f32_kernel<BM, BN, LD>), dim3(tiles), dim3(kThreads), 0, s, a);
+  const int S = a.splits > 1 ? a.splits : 1;
+  if (S > 1 && (!a.part || a.N % 4 != 0 || a.Kp / BKF < S)) return hipErrorInvalidValue;
+  hapi_launch((conv_f32_kernel<BM, BN, LD>), dim3(tiles, S), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -2121,6 +2169,13 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
       break;
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_f32_split_reduce(const ConvArgs &a, hipStream_t s) {
+  if (a.splits <= 1 || !a.part || a.N % 4 != 0) return hipErrorInvalidValue;
+  const int64_t items = (int64_t)a.M * (a.N / 4);
+  hapi_launch(f32_split_reduce_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_conv_f32(const ConvArgs &a, Loader ld, hipStream_t s) {

@@ -90,11 +90,24 @@ struct ConvArgs {
   const float *pre_scale, *pre_shift;
   // Workgroups of the persistent kernels (0: one per CU).
   int cus;
+  // fp32 only: the k-tiles split into `splits` consecutive slices computed by
+  // separate workgroups into part [splits][M][N] (float32), then summed in
+  // slice order (fixed, so results do not depend on M); splits <= 1: none.
+  float *part;
+  int splits;
 };
+// Slices of an fp32 convolution's reduction: a function of the padded K only.
+inline int f32_splits(int Kp) {
+  const int s = Kp / 512;
+  return s < 1 ? 1 : s > 8 ? 8 : s;
+}
 constexpr int kPreMax = 1024;
 
 hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s);
 hipError_t launch_conv_f32(const ConvArgs &a, Loader ld, hipStream_t s);
+// The ordered sum of an fp32 convolution's slices (a.splits > 1), then its
+// bias, residual and activation, into a.y.
+hipError_t launch_f32_split_reduce(const ConvArgs &a, hipStream_t s);
 
 // Elementwise / memory-bound kernels; `bf16` selects the activation type.
 hipError_t launch_maxpool(bool bf16, const void *x, void *y, int n, int H, int W, int C, int k,
