@@ -58,6 +58,8 @@ struct ConvSpec {
   int cin, cout, k, stride, pad;
   bool bias, bn;
   bool s2d;  // stride-2 stem on 2x2 space-to-depth cells (first layer, few channels)
+  bool nhwc8; // first layer over <= 8 channels, 9..16 taps: NHWC with 8 channel slots,
+              // k = (tap, slot), two k-tiles of 8 taps
   int K, Kp;
   int64_t raw_w, raw_b, raw_bn;  // float offsets into the raw buffer (-1: absent)
   int64_t pk_w, pk_b;            // byte offsets into the packed buffer
@@ -117,12 +119,13 @@ int analyze(const hapi_model_desc *d, Model &m) {
   int64_t raw = 0, pk = 0;
 
   auto add_conv = [&](LayerPlan &lp, int cin, int cout, int k, int s, int p, bool bias, bool bn,
-                      bool s2d = false) {
+                      bool s2d = false, bool nhwc8 = false) {
     ConvSpec c{};
     c.cin = cin; c.cout = cout; c.k = k; c.stride = s; c.pad = p; c.bias = bias; c.bn = bn;
     c.s2d = s2d;
+    c.nhwc8 = nhwc8;
     c.splits = 1;
-    c.K = s2d ? ((k + 1) / 2) * ((k + 1) / 2) * kS2DChannels : cin * k * k;
+    c.K = s2d ? ((k + 1) / 2) * ((k + 1) / 2) * kS2DChannels : nhwc8 ? 16 * 8 : cin * k * k;
     c.Kp = (c.K + kq - 1) / kq * kq;
     c.raw_w = raw; raw += (int64_t)cout * cin * k * k;
     c.raw_b = -1; c.raw_bn = -1;
@@ -182,9 +185,14 @@ int analyze(const hapi_model_desc *d, Model &m) {
         // 4 x 4 cells of 2 x 2 pixels runs on the space-to-depth layout.
         const bool s2d = first && m.bf16 && L.stride == 2 && L.cin <= 4 && (L.k + 1) / 2 == 4 &&
                          L.cout % 8 == 0;
-        add_conv(lp, L.cin, L.cout, L.k, L.stride, L.pad, L.has_bias != 0, L.has_bn != 0, s2d);
+        // Any other first layer over <= 8 channels with 9..16 taps (VGG's 3 x 3
+        // over RGB) reads an NHWC copy of its input with 8 channel slots.
+        const bool nhwc8 = first && m.bf16 && !s2d && L.cin <= 8 && L.k * L.k > 8 && L.k * L.k <= 16 &&
+                           L.cout % 8 == 0;
+        add_conv(lp, L.cin, L.cout, L.k, L.stride, L.pad, L.has_bias != 0, L.has_bn != 0, s2d, nhwc8);
         lp.out = Act{L.cout, ho, wo, false};
         if (s2d) lp.tmp_elems = (int64_t)(ho + 3) * (wo + 3) * kS2DChannels;
+        if (nhwc8) lp.tmp_elems = (int64_t)cur.h * cur.w * 8;
         if (!m.bf16 && L.cout % 4 == 0) {
           // fp32: long reductions run as slices (the slice count depends on K
           // only, so results do not depend on the batch or its partitions)
@@ -548,6 +556,11 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
     a.stride = 1;
     a.pad = 0;
     ld = LD_S2D;
+  } else if (cs.nhwc8) {
+    // x is the 8-slot NHWC copy of the input
+    a.C = 8;
+    a.kh = a.kw = cs.k;
+    ld = LD_NHWC8;
   } else if (nchw_input) {
     const bool vec_ok = c.m.bf16 && cs.k % 8 == 0 && cs.stride % 8 == 0 && cs.pad == 0 &&
                         in.w % 8 == 0 && ((uintptr_t)x % 16) == 0;
@@ -555,7 +568,8 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
   } else {
     ld = (cs.k == 1 && cs.stride == 1 && cs.pad == 0) ? LD_GEMM : LD_NHWC;
   }
-  const double flops = 2.0 * a.M * (double)a.N * (cs.s2d ? (double)cs.cin * cs.k * cs.k : (double)a.K);
+  const double flops =
+      2.0 * a.M * (double)a.N * (cs.s2d || cs.nhwc8 ? (double)cs.cin * cs.k * cs.k : (double)a.K);
   const double bytes = (double)c.m.esz * ((double)nb * in.elems() + (double)a.M * a.N * (res ? 2 : 1) +
                                           (double)a.N * a.K + (cs.fused ? (double)a.M * cs.cin2 : 0.0));
   if (c.m.bf16)
@@ -668,6 +682,12 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
                           return launch_space_to_depth(cur, c.slot[o], nb, lp.in.c, lp.in.h, lp.in.w,
                                                        cs.pad, ho + 3, wo + 3, c.s);
                         }));
+          src = c.slot[o];
+          o = free_slot(o);
+        } else if (cs.nhwc8) {
+          HIP_TRY(timed(c.s, F_LAYOUT, 0.0, (double)nb * lp.in.h * lp.in.w * (lp.in.c + 8) * m.esz, [&] {
+            return launch_nchw_to_nhwc8(cur, c.slot[o], nb, lp.in.c, lp.in.h, lp.in.w, c.s);
+          }));
           src = c.slot[o];
           o = free_slot(o);
         }
@@ -1050,7 +1070,7 @@ int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void
     const bool nchw = li == 0 && m.first_reads_nchw;
     for (const ConvSpec &c : lp.convs) {
       const float *bn = c.raw_bn >= 0 ? raw + c.raw_bn : nullptr;
-      const PackOrder order = c.s2d ? PACK_S2D : nchw ? PACK_CKHKW : PACK_KHKWC;
+      const PackOrder order = c.s2d ? PACK_S2D : c.nhwc8 ? PACK_KHKWC8 : nchw ? PACK_CKHKW : PACK_KHKWC;
       float *bias = reinterpret_cast<float *>(pk + c.pk_b);
       HIP_TRY(launch_pack_conv(m.bf16, raw + c.raw_w, c.raw_b >= 0 ? raw + c.raw_b : nullptr,
                                bn, bn ? bn + c.cout : nullptr, bn ? bn + 2 * c.cout : nullptr,

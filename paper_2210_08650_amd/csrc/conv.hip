@@ -726,7 +726,8 @@ constexpr int kStreamWorkgroups = 256;
 // chunk (l % 8) ^ ((row >> 1) & 7) of the 64-wide k-tile, as in DmaPlan.
 template <int NA, int NB, int LD, int KW>
 struct WsPlan {
-  static constexpr int TAPS = (LD == LD_NHWC || LD == LD_CAT) ? KW * KW : 1;
+  // LD_NHWC8: one offset per k-tile (two k-tiles of 8 taps each)
+  static constexpr int TAPS = (LD == LD_NHWC || LD == LD_CAT) ? KW * KW : LD == LD_NHWC8 ? 2 : 1;
   unsigned va[TAPS][NA];                // A, first part: per kernel tap
   unsigned va2[LD == LD_CAT ? NA : 1];  // LD_CAT: shortcut pixel (n, ho s2, wo s2) of x2
   unsigned vb[NB];
@@ -743,7 +744,17 @@ struct WsPlan {
       const int mm = valid ? m : 0;
       const int n = mm / hw, rem = mm - n * hw;
       const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
-      if (LD == LD_GEMM) {
+      if (LD == LD_NHWC8) {
+        // chunk kc8 / 8 of k-tile t is tap 8 t + kc8 / 8: the 8 channel slots
+        // of one input pixel, or zeros (padding, taps past kh x kw)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int tap = 8 * t + kc8 / 8;
+          const int hi = ho * a.stride - a.pad + tap / a.kw, wi = wo * a.stride - a.pad + tap % a.kw;
+          const bool in = valid && tap < a.kh * a.kw && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
+          va[t][i] = in ? (unsigned)(((((int64_t)n * a.H + hi) * a.W + wi) * 8) * 2) : kOob;
+        }
+      } else if (LD == LD_GEMM) {
         va[0][i] = valid ? (unsigned)(((int64_t)m * (a.lda ? a.lda : a.K) + kc8) * 2) : kOob;
       } else if (LD == LD_S2D) {  // k-tile du adds du * W * C (scalar)
         va[0][i] = valid ? (unsigned)(((((int64_t)n * a.H + ho) * a.W + wo) * a.C + kc8) * 2) : kOob;
@@ -832,8 +843,9 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
     Plan pl;
     pl.init(a, m0, n0, pw * NA, pw * NB, lane);
     // k-tiles per tap of the first part; the scalar A offset of k-tile (tap, cb)
-    const int cpt = (LD == LD_NHWC || LD == LD_CAT) ? a.C / BK : nk;
+    const int cpt = (LD == LD_NHWC || LD == LD_CAT) ? a.C / BK : LD == LD_NHWC8 ? 1 : nk;
     auto soff_a = [&](int cb) -> unsigned {
+      if (LD == LD_NHWC8) return 0u;
       if (LD == LD_GEMM || LD == LD_NHWC || LD == LD_CAT) return (unsigned)(cb * BK * 2);
       if (LD == LD_S2D) return (unsigned)(cb * a.W * a.C * 2);
       // LD_NCHW_PATCH: channel c = cb / (kh / 4), kernel rows u0 = 4 (cb % (kh / 4))
@@ -1760,6 +1772,8 @@ bool ws_eligible(const ConvArgs &a, Loader ld) {
       if ((int64_t)a.n_img * a.H * a.W * a.C * 2 >= lim) return false;
       return ld == LD_NHWC || (a.C2 % BK == 0 && (int64_t)a.n_img * a.H2 * a.W2 * a.C2 * 2 < lim);
     case LD_S2D: return (int64_t)a.n_img * a.H * a.W * a.C * 2 < lim;
+    case LD_NHWC8:
+      return a.Kp == 2 * BK && a.kh * a.kw > 8 && a.kh * a.kw <= 16 && (int64_t)a.n_img * a.H * a.W * 16 < lim;
     case LD_NCHW_PATCH:
       return a.kw == 16 && a.kh % 4 == 0 && (int64_t)a.n_img * a.C * a.H * a.W * 2 < lim;
     default: return false;
@@ -2167,6 +2181,10 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
     case LD_CAT:
       if (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) return launch_pipe_ld<LD_CAT>(a, s);
       break;
+    case LD_NHWC8:
+      if (a.N % 8 != 0 || a.ldc % 8 != 0 || a.ldr % 8 != 0 || !ws_eligible(a, LD_NHWC8)) break;
+      if (a.N <= 64) return launch_ws_cfg<128, 64, 2, 2, 3, LD_NHWC8, 1, 0, 2>(a, s);
+      return launch_ws_cfg<128, 128, 2, 2, 2, LD_NHWC8, 1, 0, 2>(a, s);
   }
   return hipErrorInvalidValue;
 }

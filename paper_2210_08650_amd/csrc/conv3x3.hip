@@ -1,6 +1,8 @@
 // Row-streaming 3 x 3 convolution for gfx950: stride 1, padding 1, 64 input
-// and 64 output channels, NHWC bf16, image width <= 64 (the ResNet stage-1
-// bottleneck and basic-block convolutions).
+// and 64 output channels, NHWC bf16 (the ResNet stage-1 bottleneck and
+// basic-block convolutions, VGG's second convolution).  Rows wider than 64
+// pixels are cut into strips of 64 output columns, each streamed by its own
+// workgroups with a one-column halo on either side.
 //
 // The implicit-GEMM kernels gather every k-tile of such a layer from L2 (each
 // input pixel is fetched nine times, once per tap) and are bound by the
@@ -60,6 +62,7 @@ struct Conv3Args {
   uint16_t *y;          // [n * H * W][ldc]
   int H, W, ldw, ldc, ldr, relu;
   int bands, band_rows;  // output rows [b * band_rows, ...) of each image per workgroup
+  int strips;            // 64-column strips per row: workgroup (img, band, strip)
   // Expansion (EXPAND kernels): the 3 x 3 result, with bias and ReLU and
   // rounded to bf16, is the 64-channel input of a 1 x 1 convolution to
   // kExpand channels (packed [kExpand][ldw3]) with bias3, the residual res
@@ -89,7 +92,10 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int lrow = lane & 31, lh = lane >> 5;
-  const int img = blockIdx.x / a.bands, band = blockIdx.x - img * a.bands;
+  const int per_img = a.bands * a.strips;
+  const int img = blockIdx.x / per_img, rest = blockIdx.x - img * per_img;
+  const int band = rest / a.strips, strip = rest - band * a.strips;
+  const int c0 = strip * (kPix - 2);  // first output column of the strip
   const int r0 = band * a.band_rows;
   const int r1 = min(a.H, r0 + a.band_rows);
   const int64_t img_px = (int64_t)img * a.H * a.W;
@@ -99,8 +105,8 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
   // Branch-free: a chunk outside the image reads the image's first pixel and
   // is zeroed when stored, so the loads of a whole row set stay in flight.
   auto load_row = [&](int h, int it) -> uint4 {
-    const int p = it >> 3, c = it & 7;  // ring pixel p holds column p - 1
-    const int col = p - 1;
+    const int p = it >> 3, c = it & 7;  // ring pixel p holds column c0 + p - 1
+    const int col = c0 + p - 1;
     const bool ok = it < kRowChunks && (unsigned)h < (unsigned)a.H && (unsigned)col < (unsigned)a.W;
     const int64_t pix = ok ? (int64_t)h * a.W + col : 0;
     uint4 v = *reinterpret_cast<const uint4 *>(a.x + ((img_px + pix) << 6) + c * 8);
@@ -179,9 +185,9 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
     }
     const int row = ho + (wave & (kStepRows - 1));  // this wave's output row
     const int pi = wave / kStepRows;                 // and its 32-pixel half
-    const int px = 32 * pi + lrow;
-    const int64_t m = img_px + (int64_t)row * a.W + px;
-    const bool live = row < r1 && px < a.W;
+    const int px = 32 * pi + lrow;  // ring pixel px + 1, output column c0 + px
+    const int64_t m = img_px + (int64_t)row * a.W + c0 + px;
+    const bool live = row < r1 && c0 + px < a.W;
     // EXPAND: the residual of this lane's outputs, loaded now so that its
     // latency hides behind the 3 x 3 MFMAs.  Part (h, jn, q) holds channels
     // 128 h + 32 jn + 16 q + 8 lh .. + 8 of pixel px.
@@ -260,7 +266,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
             const int n = 32 * j + 16 * q + 8 * lh;
             float v[8];
             finish8(acc[j], q, bias_s + n, v);
-            if (px < a.W) {
+            if (c0 + px < a.W) {
               if (a.res) add_res(*reinterpret_cast<const uint4 *>(a.res + m * a.ldr + n), v);
               uint32_t o[4];
 #pragma unroll
@@ -330,7 +336,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
               const int n = 128 * h + 32 * jn + 16 * q + 8 * lh;
               float v[8];
               finish8(e3[jn], q, bias3_s + n, v);
-              if (px < a.W) {
+              if (c0 + px < a.W) {
                 add_res(rr[h][jn][q], v);
                 uint32_t o[4];
 #pragma unroll
@@ -348,8 +354,8 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
 }  // namespace
 
 bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, int W, int Kp, int ldc, int ldr) {
-  return C == kC && N == kC && kh == 3 && kw == 3 && stride == 1 && pad == 1 && W >= 1 && W <= kPix - 2 &&
-         Kp == kK && ldc % 8 == 0 && ldr % 8 == 0;
+  return C == kC && N == kC && kh == 3 && kw == 3 && stride == 1 && pad == 1 && W >= 1 && Kp == kK &&
+         ldc % 8 == 0 && ldr % 8 == 0;
 }
 
 bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr) {
@@ -359,8 +365,10 @@ bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr) {
 hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float *bias, const void *res, int ldr,
                               void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s,
                               const void *w3, int ldw3, const float *bias3) {
-  // Enough workgroups to fill the CUs: split images into bands of rows.
-  int bands = (cus + n - 1) / n;
+  // Enough workgroups to fill the CUs: split images into strips of columns,
+  // then into bands of rows.
+  const int strips = (W + kPix - 3) / (kPix - 2);
+  int bands = (cus + n * strips - 1) / (n * strips);
   bands = bands < 1 ? 1 : bands;
   const int max_bands = (H + kStepRows - 1) / kStepRows;
   bands = bands > max_bands ? max_bands : bands;
@@ -369,11 +377,13 @@ hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float
   bands = (H + band_rows - 1) / band_rows;
   Conv3Args a{static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(w), bias,
               static_cast<const uint16_t *>(res), static_cast<uint16_t *>(y), H, W, ldw, ldc, ldr, relu ? 1 : 0,
-              bands, band_rows, static_cast<const uint16_t *>(w3), bias3, ldw3};
+              bands, band_rows, strips, static_cast<const uint16_t *>(w3), bias3, ldw3};
+  const int64_t grid = (int64_t)n * bands * strips;
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
   if (w3)
-    hapi_launch(conv3x3_c64_kernel<true>, dim3(n * bands), dim3(kThreads), 0, s, a);
+    hapi_launch(conv3x3_c64_kernel<true>, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
   else
-    hapi_launch(conv3x3_c64_kernel<false>, dim3(n * bands), dim3(kThreads), 0, s, a);
+    hapi_launch(conv3x3_c64_kernel<false>, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -316,6 +316,9 @@ __global__ void pack_conv_kernel(const float *__restrict__ w, const float *__res
     const int cell = k >> 4, du = cell / kw2, dv = cell % kw2;
     const int u = 2 * du + a, v = 2 * dv + b;
     if (c < C && u < kh && v < kw) val = w[(((int64_t)n * C + c) * kh + u) * kw + v] * sc;
+  } else if (order == PACK_KHKWC8) {
+    const int tap = k >> 3, c = k & 7;
+    if (c < C && tap < kh * kw) val = w[(((int64_t)n * C + c) * kh + tap / kw) * kw + tap % kw] * sc;
   } else if (k < K) {
     int c, u, v;
     if (order == PACK_CKHKW) {
@@ -361,6 +364,19 @@ __global__ void s2d_kernel(const uint16_t *__restrict__ x, uint16_t *__restrict_
                       v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
   dst[1] = make_uint4(v[8] | ((uint32_t)v[9] << 16), v[10] | ((uint32_t)v[11] << 16),
                       v[12] | ((uint32_t)v[13] << 16), v[14] | ((uint32_t)v[15] << 16));
+}
+
+// NCHW (C <= 8) -> NHWC with 8 channel slots: one thread per pixel (16 bytes).
+__global__ void nhwc8_kernel(const uint16_t *__restrict__ x, uint16_t *__restrict__ y, int n, int C,
+                             int64_t HW) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)n * HW) return;
+  const int64_t img = i / HW, p = i - img * HW;
+  uint32_t v[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) v[c] = c < C ? x[(img * C + c) * HW + p] : 0u;
+  *reinterpret_cast<uint4 *>(y + i * 8) =
+      make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
 // Concatenation along channels: one thread per 8 channels (16 bytes).
@@ -433,6 +449,14 @@ hipError_t launch_affine(const void *x, const float *scale, const float *shift, 
 hipError_t launch_pack_affine(const float *bn, int C, float *scale, float *shift, hipStream_t s) {
   hapi_launch(pack_affine_kernel, dim3(blocks_for(C, 256)), dim3(256), 0, s, bn, C, scale,
                      shift);
+  return hipGetLastError();
+}
+
+hipError_t launch_nchw_to_nhwc8(const void *x, void *y, int n, int C, int H, int W, hipStream_t s) {
+  if (C < 1 || C > 8) return hipErrorInvalidValue;
+  const int64_t total = (int64_t)n * H * W;
+  hapi_launch(nhwc8_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s, (const uint16_t *)x, (uint16_t *)y, n,
+              C, (int64_t)H * W);
   return hipGetLastError();
 }
 

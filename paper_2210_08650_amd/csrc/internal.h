@@ -53,15 +53,19 @@ enum Loader : int {
   LD_NCHW_PATCH = 3, // NCHW images, non-overlapping patches with k % 8 == 0 (bf16)
   LD_S2D = 4,        // space-to-depth cells (see launch_space_to_depth): every k-tile
                      // is one contiguous 64-element run, zero border, no bounds checks
-  LD_CAT = 5         // two sources along K: k < K1 as LD_NHWC over x, k >= K1 a 1x1
+  LD_CAT = 5,        // two sources along K: k < K1 as LD_NHWC over x, k >= K1 a 1x1
                      // convolution with stride s2 over x2 (a residual block's shortcut)
+  LD_NHWC8 = 6       // NHWC with 8 channel slots per pixel (C <= 8, zero padded; see
+                     // launch_nchw_to_nhwc8): k = (tap, c8), a 64-wide k-tile holds 8
+                     // taps, 9 .. 16 taps in two k-tiles (first layers over images)
 };
 
 // Weight order of a packed convolution.
 enum PackOrder : int {
   PACK_KHKWC = 0,  // k = (kh, kw, c)       NHWC inputs
   PACK_CKHKW = 1,  // k = (c, kh, kw)       NCHW inputs
-  PACK_S2D = 2     // k = (du, dv, a, b, c4) stride-2 convolution on 2x2 cells
+  PACK_S2D = 2,    // k = (du, dv, a, b, c4) stride-2 convolution on 2x2 cells
+  PACK_KHKWC8 = 3  // k = (kh, kw, c8): 8 channel slots per tap (LD_NHWC8)
 };
 
 // One convolution / linear layer as an implicit GEMM:
@@ -139,6 +143,9 @@ hipError_t launch_pack_conv(bool bf16, const float *w, const float *conv_bias, c
 // Space-to-depth for a stride-2 convolution with C <= 4 input channels:
 // y[n][P][Q][(a*2 + b)*4 + c] = x[n][c][2P + a - pad][2Q + b - pad] (0 outside
 // the image or for c >= C), P < HP, Q < WP.  bf16 only.
+// NCHW bf16 images with C <= 8 channels -> NHWC with 8 channel slots per
+// pixel, the slots past C zero: y[n][h][w][0..7].
+hipError_t launch_nchw_to_nhwc8(const void *x, void *y, int n, int C, int H, int W, hipStream_t s);
 hipError_t launch_space_to_depth(const void *x, void *y, int n, int C, int H, int W, int pad,
                                  int HP, int WP, hipStream_t s);
 constexpr int kS2DChannels = 16;

@@ -41,7 +41,11 @@ def _int_conv_case(seed, dtype, pre_pool, C, N, k, s, p, HW, batch, relu=True, l
 # (pre_pool, C, N, k, s, p, HW, batch): pre_pool routes the conv through the
 # NHWC loaders (a 1x1 identity pool first); otherwise it reads NCHW images.
 BF16_CASES = [
-    (False, 3, 64, 3, 1, 1, 23, 3),      # NCHW gather, K = 27 padded to 64, ragged M
+    (False, 3, 64, 3, 1, 1, 23, 3),      # 8-slot NHWC: two k-tiles of 8 taps, ragged M
+    (False, 3, 64, 3, 1, 1, 224, 2),     # VGG's first layer at full resolution
+    (False, 1, 128, 3, 2, 1, 31, 3),     # 8-slot NHWC, one channel, stride 2, 128-wide tile
+    (False, 8, 40, 4, 1, 2, 19, 2),      # 8-slot NHWC, 16 taps, 8 channels, ragged N tile
+    (False, 3, 64, 5, 1, 2, 23, 3),      # NCHW gather, K = 75 padded to 128, ragged M
     (False, 3, 64, 7, 2, 3, 37, 2),      # stem geometry on space-to-depth cells
     (False, 3, 64, 7, 2, 3, 224, 2),     # the ResNet stem at full resolution
     (False, 4, 32, 8, 2, 3, 29, 3),      # space-to-depth with 4 channels, k = 8, N = 32
@@ -55,7 +59,9 @@ BF16_CASES = [
     (True, 64, 256, 1, 1, 0, 128, 4),    # M = 65536: 256 x 128 tiles
     (True, 64, 64, 3, 1, 1, 56, 2),      # row-streaming 3x3, 64 -> 64 (ResNet stage 1)
     (True, 64, 64, 3, 1, 1, 17, 3),      # row-streaming 3x3, ragged rows and bands
-    (True, 64, 64, 3, 1, 1, 64, 1),      # row-streaming 3x3 at its widest row
+    (True, 64, 64, 3, 1, 1, 64, 1),      # row-streaming 3x3: one full 64-column strip
+    (True, 64, 64, 3, 1, 1, 130, 2),     # row-streaming 3x3: three strips, the last 2 columns wide
+    (True, 64, 64, 3, 1, 1, 224, 1),     # VGG's second layer: four 64-column strips
     (True, 128, 32, 3, 1, 1, 15, 3),     # 32 output channels, few rows: 128 x 64 tiles
     (True, 128, 32, 3, 1, 1, 256, 2),    # 32 output channels, M = 131072: 256 x 32 tiles
     (True, 128, 24, 3, 1, 1, 256, 2),    # 24 output channels in a 32-column tile
@@ -125,7 +131,7 @@ def test_identity_kernel_conv_is_exact_on_random_values():
         assert np.array_equal(r2.extract_np(xd, 2), xv[:, :, ::2, ::2])
 
 
-@pytest.mark.parametrize("hw,batch", [(20, 3), (56, 2), (9, 2)])
+@pytest.mark.parametrize("hw,batch", [(20, 3), (56, 2), (9, 2), (70, 1)])
 def test_fused_bottleneck_block_exact(hw, batch):
     """A stage-1 bottleneck with an identity shortcut runs its 3x3 and its
     expanding 1x1 convolution as one kernel (the 3x3 result stays on chip,
