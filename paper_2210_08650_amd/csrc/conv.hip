@@ -1055,10 +1055,18 @@ __global__ __launch_bounds__(2 * WM * WN * 64, 2) void conv_bf16_ws2_kernel(Conv
   conv_bf16_ws_body<BM, BN, WM, WN, STAGES, LD, KW, EPI, PRE>(a);
 }
 
+template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI>
+__global__ __launch_bounds__(2 * WM * WN * 64, 3) void conv_bf16_ws3_kernel(ConvArgs a) {
+  conv_bf16_ws_body<BM, BN, WM, WN, STAGES, LD, KW, EPI>(a);
+}
+
 template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 0, int MINB = 1, bool PRE = false>
 hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  if constexpr (MINB >= 2)
+  if constexpr (MINB >= 3 && !PRE)
+    hapi_launch((conv_bf16_ws3_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
+                       dim3(2 * WM * WN * 64), 0, s, a);
+  else if constexpr (MINB >= 2)
     hapi_launch((conv_bf16_ws2_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI, PRE>), dim3(tiles),
                        dim3(2 * WM * WN * 64), 0, s, a);
   else
@@ -1833,6 +1841,10 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     case 46: return launch_pws_ld<256, 64, 8, 1, 4, 3, LD, 2>(a, s);
     case 47: return launch_pws_ld<256, 128, 4, 2, 4, 2, LD, 2>(a, s);
     case 57: return launch_ws_ld<256, 32, 4, 1, 2, LD, 0, 2>(a, s);
+    case 58: return launch_ws_ld<64, 64, 2, 2, 4, LD, 0, 2>(a, s);
+    case 59: return launch_ws_ld<64, 64, 2, 2, 3, LD, 0, 3>(a, s);
+    case 60: return launch_ws_ld<64, 128, 2, 2, 3, LD, 0, 2>(a, s);
+    case 61: return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
     case 50: if (a.Kp <= 2 * BK) return launch_short_ld<128, 128, 2, 2, LD, 3>(a, s); break;
     case 51: if (a.Kp <= 2 * BK) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s); break;
     case 52: if (a.Kp <= 2 * BK) return launch_short_ld<64, 128, 2, 2, LD, 4>(a, s); break;
@@ -1843,9 +1855,12 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
   // Measured on MI355X over the ResNet-50 conv shapes (per-layer kernel
   // traces of every configuration above):
   // - the warp-specialised kernel with two workgroups per CU (128 x 64 tiles)
-  //   for the space-to-depth stem, 64-channel outputs with K = 64 or K >= 512,
-  //   and residual layers with >= 1024 output channels; with 128 x 128 tiles
-  //   for the other residual layers and for 128-channel outputs with K > 256;
+  //   for the space-to-depth stem and 64-channel outputs with K = 64 or
+  //   K >= 512; with 128 x 128 tiles for residual layers with < 1024 output
+  //   channels and for 128-channel 3 x 3 layers; with three workgroups per CU
+  //   (128 x 64 tiles, two stages: more loads in flight for these
+  //   latency-bound layers) for residual layers with >= 1024 output channels
+  //   and 128-channel 1 x 1 layers with K >= 512;
   // - the persistent kernel (one workgroup of 8 consumer and 4 producer waves
   //   per CU) with 128 x 256 tiles for the fused shortcut GEMMs and the other
   //   layers, and with 256 x 128 tiles for 128-channel 1 x 1 layers with short
@@ -1868,13 +1883,14 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
       if (a.K >= 512 || a.K == BK) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
     } else if (a.res) {
       if (a.K >= 2 * BK) {
-        if (a.N >= 1024) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+        if (a.N >= 1024) return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
         return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
       }
     } else if (LD == LD_CAT) {
       return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
     } else if (a.N <= 128) {
       if (a.kh == 1 && a.K <= 256 && a.K >= 2 * BK) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
+      if (a.kh == 1 && a.K >= 512) return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
       if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
     } else if (a.N >= 512 && a.K >= 2048) {
       return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);

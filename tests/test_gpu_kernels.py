@@ -56,6 +56,7 @@ BF16_CASES = [
     (True, 128, 192, 3, 2, 1, 17, 2),    # NHWC 3x3 / 2, N = 192
     (True, 64, 256, 1, 2, 0, 14, 3),     # 1x1 / 2 shortcut geometry
     (True, 128, 64, 1, 1, 0, 21, 2),     # GEMM loader, N = 64 tile
+    (True, 512, 128, 1, 1, 0, 14, 2),    # 1x1, K = 512: three workgroups per CU, two stages
     (True, 64, 256, 1, 1, 0, 128, 4),    # M = 65536: 256 x 128 tiles
     (True, 64, 64, 3, 1, 1, 56, 2),      # row-streaming 3x3, 64 -> 64 (ResNet stage 1)
     (True, 64, 64, 3, 1, 1, 17, 3),      # row-streaming 3x3, ragged rows and bands
