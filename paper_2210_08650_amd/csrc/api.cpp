@@ -657,7 +657,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
     HIP_TRY(timed(c.s, F_CONV_BF16, flops, bytes, [&] {
       return launch_stem_pool_bf16(images, c.pk + cs.pk_w, cs.Kp, reinterpret_cast<const float *>(c.pk + cs.pk_b),
                                    c.slot[o], nb, l0.in.c, l0.in.h, l0.in.w, l0.out.h, l0.out.w, l1.out.h,
-                                   l1.out.w, c.s);
+                                   l1.out.w, c.cus, c.s);
     }));
     cur = c.slot[o];
     cur_slot = o;

@@ -170,7 +170,7 @@ bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr);
 int cu_count();
 bool stem_pool_supported(int C, int H, int W, int cout, int Ho, int Wo, int Hp, int Wp);
 hipError_t launch_stem_pool_bf16(const void *x, const void *w, int ldw, const float *bias, void *y, int n, int C,
-                                 int H, int W, int Ho, int Wo, int Hp, int Wp, hipStream_t s);
+                                 int H, int W, int Ho, int Wo, int Hp, int Wp, int cus, hipStream_t s);
 hipError_t launch_copy_f32(const float *x, float *y, int64_t n, hipStream_t s);
 // Channel-slice copy (concatenation): y[p * cy + off + c] = x[p * cx + c], c < C,
 // for `pixels` NHWC pixels.  C, cx, cy, off multiples of 8.  bf16.

@@ -16,8 +16,9 @@
 //   horizontal maxima are formed in registers (half-wave exchanges and one
 //   edge pixel through LDS), and a running vertical maximum emits every
 //   pooled row as soon as its three conv rows are done.
-// One workgroup of 4 waves handles half an image (a band of pooled rows);
-// wave w computes conv pixels [32 w, 32 w + 32) of every conv row.
+// One workgroup of 4 waves handles a band of pooled rows of one image (two
+// bands per image, more when the batch is too small to fill the CUs); wave w
+// computes conv pixels [32 w, 32 w + 32) of every conv row of the band.
 #include <cstdint>
 
 #include "internal.h"
@@ -43,6 +44,7 @@ struct StemArgs {
   uint16_t *y;        // [n, Hp, Wp, 64] pooled output (NHWC)
   int n, C, H, W, ldw;
   int Ho, Wo, Hp, Wp;
+  int bands;  // bands of pooled rows per image
 };
 
 // Cell (P, Q) of image img: element (a * 2 + b) * 4 + c is input pixel
@@ -95,9 +97,9 @@ __global__ __launch_bounds__(64 * kStemWaves, 2) void stem_pool_kernel(StemArgs 
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int lrow = lane & 31, lh = lane >> 5;
-  const int img = blockIdx.x >> 1, half = blockIdx.x & 1;
+  const int img = blockIdx.x / a.bands, band = blockIdx.x - img * a.bands;
   // Pooled rows [p0, p1) of this image; pooled row i takes conv rows 2i-1 .. 2i+1.
-  const int p0 = half ? a.Hp / 2 : 0, p1 = half ? a.Hp : a.Hp / 2;
+  const int p0 = band * a.Hp / a.bands, p1 = (band + 1) * a.Hp / a.bands;
   const int r0 = p0 > 0 ? 2 * p0 - 1 : 0, r1 = 2 * p1;  // conv rows [r0, r1)
   const int plast = r1 - 1 + 3;                          // last cell row needed
 
@@ -251,10 +253,17 @@ bool stem_pool_supported(int C, int H, int W, int cout, int Ho, int Wo, int Hp, 
 }
 
 hipError_t launch_stem_pool_bf16(const void *x, const void *w, int ldw, const float *bias, void *y, int n, int C,
-                                 int H, int W, int Ho, int Wo, int Hp, int Wp, hipStream_t s) {
+                                 int H, int W, int Ho, int Wo, int Hp, int Wp, int cus, hipStream_t s) {
+  // Two bands per image, or enough for one workgroup per CU, with at least
+  // four pooled rows per band (each band recomputes one conv row of halo).
+  int bands = n > 0 ? (cus + n - 1) / n : 2;
+  bands = bands < 2 ? 2 : bands;
+  const int max_bands = Hp / 4 < 2 ? 2 : Hp / 4;
+  bands = bands > max_bands ? max_bands : bands;
+  bands = bands > Hp ? Hp : bands;
   StemArgs a{static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(w), bias, static_cast<uint16_t *>(y),
-             n, C, H, W, ldw, Ho, Wo, Hp, Wp};
-  hapi_launch(stem_pool_kernel, dim3(2 * n), dim3(64 * kStemWaves), 0, s, a);
+             n, C, H, W, ldw, Ho, Wo, Hp, Wp, bands};
+  hapi_launch(stem_pool_kernel, dim3(bands * n), dim3(64 * kStemWaves), 0, s, a);
   return hipGetLastError();
 }
 
