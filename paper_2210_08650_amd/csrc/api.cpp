@@ -497,6 +497,7 @@ struct Ctx {
   std::function<void(int, bool)> on_layer;  // (layer index, begin) for profiling
   int cus;      // workgroups of persistent kernels
   float *part;  // fp32 partial sums of split reductions
+  int lanes;    // partitions in flight
 };
 
 // Per-channel scale and shift (an inference batch-norm) that a 1 x 1
@@ -512,6 +513,7 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
                     const void *x2 = nullptr, const Act *in2 = nullptr, PreAct pre = PreAct{}) {
   ConvArgs a{};
   a.cus = c.cus;
+  a.lanes = c.lanes;
   a.pre_scale = pre.scale;
   a.pre_shift = pre.shift;
   a.lda = pre.lda;
@@ -977,7 +979,8 @@ int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, con
   for (int i = 0; i < lanes; ++i) {
     uint8_t *w0 = ws + (int64_t)i * lane_bytes;
     c.push_back(Ctx{m, i ? L->aux[i - 1] : s, static_cast<const uint8_t *>(weights),
-                    {w0, w0 + sb, w0 + 2 * sb}, on_layer, cus, reinterpret_cast<float *>(w0 + 3 * sb)});
+                    {w0, w0 + sb, w0 + 2 * sb}, on_layer, cus, reinterpret_cast<float *>(w0 + 3 * sb),
+                    std::min(lanes, (batch + chunk - 1) / chunk)});
   }
   const int64_t in_bytes = act_at(m, start).elems() * m.esz;
   const int64_t out_bytes = m.layers[split - 1].out.elems() * m.esz;

@@ -1874,6 +1874,14 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
   if (LD == LD_GEMM && a.Kp == 2 * BK && a.N == 512 && a.res) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s);
   if (ws_eligible(a, (Loader)LD)) {
     if (LD == LD_S2D) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+    // Long reductions whose 256-row tiles cannot fill the CUs, with no other
+    // partition in flight to fill them: persistent 128 x 128 tiles (twice the
+    // tiles; ResNet-18 b64 stage 3: 111 -> 82 us, ResNet-50 b32: 31.8k ->
+    // 37.4k images/s).  With two partitions in flight the larger tiles stay
+    // faster (ResNet-50 b256: 70.1k against 67.2k images/s).
+    if (a.lanes <= 1 && a.N >= 128 && a.K >= 1024 &&
+        (int64_t)((a.M + 255) / 256) * ((a.N + 127) / 128) < a.cus)
+      return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 2>(a, s);
     // 32 output channels (DenseNet growth): a 32-column tile, so no MFMA
     // works on padding; 64 x 32 per consumer wave.  Only with >= 512 tiles:
     // with fewer the 256-row tiles leave CUs idle (measured: DenseNet-121
@@ -1887,6 +1895,7 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
         return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
       }
     } else if (LD == LD_CAT) {
+      if (a.N <= 128) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
       return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
     } else if (a.N <= 128) {
       if (a.kh == 1 && a.K <= 256 && a.K >= 2 * BK) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);

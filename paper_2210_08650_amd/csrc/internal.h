@@ -94,6 +94,9 @@ struct ConvArgs {
   const float *pre_scale, *pre_shift;
   // Workgroups of the persistent kernels (0: one per CU).
   int cus;
+  // Partitions in flight on the device (kernels of the others may fill the
+  // CUs this launch leaves idle); tile choice only, never the results.
+  int lanes;
   // fp32 only: the k-tiles split into `splits` consecutive slices computed by
   // separate workgroups into part [splits][M][N] (float32), then summed in
   // slice order (fixed, so results do not depend on M); splits <= 1: none.
