@@ -1879,6 +1879,11 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     // tiles; ResNet-18 b64 stage 3: 111 -> 82 us, ResNet-50 b32: 31.8k ->
     // 37.4k images/s).  With two partitions in flight the larger tiles stay
     // faster (ResNet-50 b256: 70.1k against 67.2k images/s).
+    // Fewer 128 x 128 tiles than half the CUs: 64 x 64 tiles, four stages
+    // (ResNet-50 b8: 706 -> 528 us of convolutions per pass; b32 stage 4:
+    // 3 x 3s 30 -> 20 us).
+    if (a.lanes <= 1 && a.N >= 64 && 2 * (int64_t)((a.M + 127) / 128) * ((a.N + 127) / 128) < a.cus)
+      return launch_ws_ld<64, 64, 2, 2, 4, LD, 0, 2>(a, s);
     if (a.lanes <= 1 && a.N >= 128 && a.K >= 1024 &&
         (int64_t)((a.M + 255) / 256) * ((a.N + 127) / 128) < a.cus)
       return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 2>(a, s);
