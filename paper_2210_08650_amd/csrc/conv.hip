@@ -2212,6 +2212,7 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
       if (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) return launch_pipe_ld<LD_CAT>(a, s);
       break;
     case LD_NHWC8:
+      if (forced_cfg() < 0 && conv_first_supported(a)) return launch_conv_first(a, s);
       if (a.N % 8 != 0 || a.ldc % 8 != 0 || a.ldr % 8 != 0 || !ws_eligible(a, LD_NHWC8)) break;
       if (a.N <= 64) return launch_ws_cfg<128, 64, 2, 2, 3, LD_NHWC8, 1, 0, 2>(a, s);
       return launch_ws_cfg<128, 128, 2, 2, 2, LD_NHWC8, 1, 0, 2>(a, s);

@@ -169,6 +169,10 @@ hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float
                               void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s,
                               const void *w3 = nullptr, int ldw3 = 0, const float *bias3 = nullptr);
 bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr);
+// First layer over an 8-slot NHWC input (LD_NHWC8) with 64 outputs, no
+// residual: weights in registers, operands loaded straight from memory.
+bool conv_first_supported(const ConvArgs &a);
+hipError_t launch_conv_first(const ConvArgs &a, hipStream_t s);
 // Compute units of the current device.
 int cu_count();
 bool stem_pool_supported(int C, int H, int W, int cout, int Ho, int Wo, int Hp, int Wp);

@@ -41,10 +41,12 @@ def _int_conv_case(seed, dtype, pre_pool, C, N, k, s, p, HW, batch, relu=True, l
 # (pre_pool, C, N, k, s, p, HW, batch): pre_pool routes the conv through the
 # NHWC loaders (a 1x1 identity pool first); otherwise it reads NCHW images.
 BF16_CASES = [
-    (False, 3, 64, 3, 1, 1, 23, 3),      # 8-slot NHWC: two k-tiles of 8 taps, ragged M
+    (False, 3, 64, 3, 1, 1, 23, 3),      # first-layer kernel (8-slot NHWC, weights in registers), ragged row
     (False, 3, 64, 3, 1, 1, 224, 2),     # VGG's first layer at full resolution
-    (False, 1, 128, 3, 2, 1, 31, 3),     # 8-slot NHWC, one channel, stride 2, 128-wide tile
-    (False, 8, 40, 4, 1, 2, 19, 2),      # 8-slot NHWC, 16 taps, 8 channels, ragged N tile
+    (False, 3, 64, 3, 2, 1, 31, 3),      # first-layer kernel, stride 2
+    (False, 8, 64, 4, 1, 2, 19, 2),      # first-layer kernel, 16 taps (eight k-steps), 8 channels
+    (False, 1, 128, 3, 2, 1, 31, 3),     # 8-slot NHWC on the implicit GEMM, one channel, stride 2
+    (False, 8, 40, 4, 1, 2, 19, 2),      # 8-slot NHWC on the implicit GEMM, 16 taps, ragged N tile
     (False, 3, 64, 5, 1, 2, 23, 3),      # NCHW gather, K = 75 padded to 128, ragged M
     (False, 3, 64, 7, 2, 3, 37, 2),      # stem geometry on space-to-depth cells
     (False, 3, 64, 7, 2, 3, 224, 2),     # the ResNet stem at full resolution
