@@ -8,7 +8,7 @@
 // whole packed weight matrix [64][k] in registers as MFMA A fragments and
 // walks an output row 32 pixels at a time: each lane loads the 16-byte slot
 // chunk of its pixel under two kernel taps per k-step straight from global
-// memory (one B fragment), so no LDS is used at all.
+// memory (one B fragment); LDS only stages the output for whole-pixel stores.
 //
 // Reduction order: k = (tap, slot) in sequence, 16 columns (two taps) per
 // MFMA step, as the implicit-GEMM kernels run it; their further k-steps only
@@ -16,7 +16,7 @@
 // Operands are swapped (weights as A) so a lane's accumulators hold 4
 // consecutive channels of one pixel; half-wave exchanges give each lane 8
 // consecutive channels, stored as 16-byte chunks after bias, ReLU and one
-// rounding.
+// rounding, staged through LDS so that stores cover whole pixels.
 #include <cstdint>
 
 #include "internal.h"
@@ -36,6 +36,10 @@ __global__ __launch_bounds__(64 * kFirstWaves) void conv_first_kernel(ConvArgs a
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lrow = lane & 31, lh = lane >> 5;
+  // Each wave's 32 x 64 output block is staged here so that every store
+  // instruction writes 8 whole pixels (1 KB contiguous): chunk c (8
+  // channels) of pixel p sits at p * 8 + (c ^ (p & 7)).
+  __shared__ uint4 stage[kFirstWaves][32 * 8];
   const int64_t row = (int64_t)blockIdx.x * kFirstWaves + wave;  // (image, output row)
   if (row >= (int64_t)a.n_img * a.Ho) return;
   const int img = (int)(row / a.Ho), ho = (int)(row - (int64_t)img * a.Ho);
@@ -105,8 +109,6 @@ __global__ __launch_bounds__(64 * kFirstWaves) void conv_first_kernel(ConvArgs a
     }
     // acc[j][4 g + e] = channel 32 j + 8 g + 4 (lane / 32) + e of pixel wo0 + lane % 32;
     // after the exchange of part q a lane owns channels 32 j + 16 q + 8 (lane / 32) .. + 8.
-    const int wo = wo0 + lrow;
-    const int64_t m = row * a.Wo + wo;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -123,9 +125,24 @@ __global__ __launch_bounds__(64 * kFirstWaves) void conv_first_kernel(ConvArgs a
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           o[e] = a.relu ? f2bf2(fmaxf(v[2 * e], 0.0f), fmaxf(v[2 * e + 1], 0.0f)) : f2bf2(v[2 * e], v[2 * e + 1]);
-        if (wo < a.Wo)
-          *reinterpret_cast<uint4 *>(y + m * a.ldc + 32 * j + 16 * q + 8 * lh) = make_uint4(o[0], o[1], o[2], o[3]);
+        const int c = 4 * j + 2 * q + lh;
+        stage[wave][lrow * 8 + (c ^ (lrow & 7))] = make_uint4(o[0], o[1], o[2], o[3]);
       }
+    // The wave's LDS accesses complete in order; the fences keep the compiler
+    // from moving the reads above the other lanes' writes (and the next
+    // block's writes above these reads).
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int p = (lane >> 3) + 8 * i, c = lane & 7;
+      const uint4 v = stage[wave][p * 8 + (c ^ (p & 7))];
+      if (wo0 + p < a.Wo) *reinterpret_cast<uint4 *>(y + (row * a.Wo + wo0 + p) * a.ldc + 8 * c) = v;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int s = 0; s < KS; ++s) cur[s] = nxt[s];
   }
