@@ -14,7 +14,10 @@
 // Every output element's reduction visits the k-tiles in order and, inside a
 // tile, the MFMA k-steps in order, independent of the tile shape (BM, BN) and
 // of M.  Results are therefore bit-identical for any batch split.
+#include <cstdio>
 #include <cstdlib>
+#include <cstring>
+#include <vector>
 
 #include <type_traits>
 #include <utility>
@@ -1806,11 +1809,31 @@ int forced_cfg() {
   return v;
 }
 
+// Tuning override per shape: HAPI_CFG_FOR="N:K:index,..." forces a tile
+// configuration on the layers with N outputs and reduction length K.
+int shape_cfg(const ConvArgs &a) {
+  struct Rule { int n, k, cfg; };
+  static const std::vector<Rule> rules = [] {
+    std::vector<Rule> r;
+    const char *e = getenv("HAPI_CFG_FOR");
+    while (e && *e) {
+      Rule x{};
+      if (sscanf(e, "%d:%d:%d", &x.n, &x.k, &x.cfg) == 3) r.push_back(x);
+      e = strchr(e, ',');
+      if (e) ++e;
+    }
+    return r;
+  }();
+  for (const Rule &x : rules)
+    if (x.n == a.N && x.k == a.K) return x.cfg;
+  return -1;
+}
+
 // Tile shape per layer.  Every shape uses the same k-tile and MFMA, so the
 // choice never changes a result bit.
 template <int LD>
 hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
-  const int fc = forced_cfg();
+  const int fc = forced_cfg() >= 0 ? forced_cfg() : shape_cfg(a);
   if (fc >= 20 && !ws_eligible(a, (Loader)LD)) return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);
   switch (fc) {
     case 0: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);

@@ -48,6 +48,7 @@ def test_every_split_matches_oracle(name, batch):
 
 
 @pytest.mark.parametrize("name,split,chunks", [("resnet18", 8, (1, 2, 5)),
+                                                ("resnet50", 18, (1, 2)),
                                                 ("densenet121", 12, (2,)),
                                                 ("alexnet", 8, (1, 3)),
                                                 ("vit_b16", 4, (1, 3))])
