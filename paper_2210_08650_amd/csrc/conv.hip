@@ -152,7 +152,7 @@ __global__ __launch_bounds__(kThreads) void conv_bf16_kernel(ConvArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM + BN) * LDSW];
 
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = a.rev ? (int)gridDim.x - 1 - xcd_remap(blockIdx.x, gridDim.x) : xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const int t = threadIdx.x;
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   __shared__ __attribute__((aligned(16))) float pre_s[PRE ? 2 * kPreMax : 4];
 
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = a.rev ? (int)gridDim.x - 1 - xcd_remap(blockIdx.x, gridDim.x) : xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -802,7 +802,7 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   __shared__ __attribute__((aligned(16))) float pre_s[PRE ? 2 * kPreMax : 4];
 
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = a.rev ? (int)gridDim.x - 1 - xcd_remap(blockIdx.x, gridDim.x) : xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // uniform: keeps LDS addresses scalar
@@ -1173,7 +1173,8 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
         __builtin_amdgcn_s_barrier();
       }
     };
-    for (int tile = t_lo; tile < t_hi; ++tile) {
+    for (int ti = t_lo; ti < t_hi; ++ti) {
+      const int tile = a.rev ? t_lo + t_hi - 1 - ti : ti;
       const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
       Plan pl;
       pl.init(a, m0, n0, pw * NA, pw * NB, lane);
@@ -1251,7 +1252,8 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
   constexpr int NPART = EP == 2 ? 2 : 4;
   using ResT = typename std::conditional<EP == 2, uint4, uint2>::type;
   int q = 0;
-  for (int tile = t_lo; tile < t_hi; ++tile) {
+  for (int ti = t_lo; ti < t_hi; ++ti) {
+    const int tile = a.rev ? t_lo + t_hi - 1 - ti : ti;
     const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
     const int mw = m0 + wm * TM * 32, nw = n0 + wn * kWC;  // origin of this wave's block
     ResT rr[TM][TN][NPART];
@@ -1414,7 +1416,7 @@ __global__ __launch_bounds__(WM * WN * 64, MINB) void conv_bf16_short_kernel(Con
   __shared__ __attribute__((aligned(16))) float bias_s[BN];
 
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = a.rev ? (int)gridDim.x - 1 - xcd_remap(blockIdx.x, gridDim.x) : xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -1997,7 +1999,7 @@ __global__ __launch_bounds__(kThreads) void conv_f32_kernel(ConvArgs a) {
   __shared__ __attribute__((aligned(16))) float smem[2 * (BM + BN) * LDSF];
 
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = a.rev ? (int)gridDim.x - 1 - xcd_remap(blockIdx.x, gridDim.x) : xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const int t = threadIdx.x;

@@ -94,6 +94,8 @@ struct ConvArgs {
   const float *pre_scale, *pre_shift;
   // Workgroups of the persistent kernels (0: one per CU).
   int cus;
+  // Tiles in reverse order (results do not depend on the order).
+  int rev;
   // Partitions in flight on the device (kernels of the others may fill the
   // CUs this launch leaves idle); tile choice only, never the results.
   int lanes;
