@@ -1870,6 +1870,9 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     case 59: return launch_ws_ld<64, 64, 2, 2, 3, LD, 0, 3>(a, s);
     case 60: return launch_ws_ld<64, 128, 2, 2, 3, LD, 0, 2>(a, s);
     case 61: return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
+    case 62: return launch_ws_ld<128, 32, 4, 1, 2, LD, 0, 2>(a, s);
+    case 63: return launch_ws_ld<128, 32, 4, 1, 2, LD, 0, 3>(a, s);
+    case 64: return launch_ws_ld<128, 32, 4, 1, 3, LD, 0, 2>(a, s);
     case 50: if (a.Kp <= 2 * BK) return launch_short_ld<128, 128, 2, 2, LD, 3>(a, s); break;
     case 51: if (a.Kp <= 2 * BK) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s); break;
     case 52: if (a.Kp <= 2 * BK) return launch_short_ld<64, 128, 2, 2, LD, 4>(a, s); break;
@@ -1913,10 +1916,10 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
         (int64_t)((a.M + 255) / 256) * ((a.N + 127) / 128) < a.cus)
       return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 2>(a, s);
     // 32 output channels (DenseNet growth): a 32-column tile, so no MFMA
-    // works on padding; 64 x 32 per consumer wave.  Only with >= 512 tiles:
-    // with fewer the 256-row tiles leave CUs idle (measured: DenseNet-121
-    // b256 dense-block 3x3s 2,015 -> 1,840 us with this bound, 2,102 without).
-    if (a.N <= 32 && a.K >= 2 * BK && a.M >= 512 * 256) return launch_ws_ld<256, 32, 4, 1, 2, LD, 0, 2>(a, s);
+    // works on padding; 32 x 32 per consumer wave, three stages (DenseNet-121
+    // b256: 56.8k -> 57.7k img/s against 256 x 32 tiles for large M and
+    // 128 x 64 tiles, half of them padding, for small M).
+    if (a.N <= 32 && a.K >= 2 * BK) return launch_ws_ld<128, 32, 4, 1, 3, LD, 0, 2>(a, s);
     if (a.N <= 64) {
       if (a.K >= 512 || a.K == BK) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
     } else if (a.res) {

@@ -65,8 +65,8 @@ BF16_CASES = [
     (True, 64, 64, 3, 1, 1, 64, 1),      # row-streaming 3x3: one full 64-column strip
     (True, 64, 64, 3, 1, 1, 130, 2),     # row-streaming 3x3: three strips, the last 2 columns wide
     (True, 64, 64, 3, 1, 1, 224, 1),     # VGG's second layer: four 64-column strips
-    (True, 128, 32, 3, 1, 1, 15, 3),     # 32 output channels, few rows: 128 x 64 tiles
-    (True, 128, 32, 3, 1, 1, 256, 2),    # 32 output channels, M = 131072: 256 x 32 tiles
+    (True, 128, 32, 3, 1, 1, 15, 3),     # 32 output channels, few rows: 128 x 32 tiles, ragged M
+    (True, 128, 32, 3, 1, 1, 256, 2),    # 32 output channels, M = 131072: 128 x 32 tiles
     (True, 128, 24, 3, 1, 1, 256, 2),    # 24 output channels in a 32-column tile
 ]
 
