@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstdlib>
 
 #include "hapi.h"
 
@@ -107,8 +108,11 @@ struct ConvArgs {
 };
 // Slices of an fp32 convolution's reduction: a function of the padded K only.
 inline int f32_splits(int Kp) {
-  const int s = Kp / 512;
-  return s < 1 ? 1 : s > 8 ? 8 : s;
+  // One slice per 256 k (16 k-tiles), at most 16: AlexNet b4 23.2k -> 25.5k
+  // img/s against one per 512 (at most 8); one per 128 is slower again (the
+  // partial sums' traffic).
+  const int s = Kp / 256;
+  return s < 1 ? 1 : s > 16 ? 16 : s;
 }
 constexpr int kPreMax = 1024;
 

@@ -82,8 +82,8 @@ F32_CASES = [
     (True, 64, 192, 5, 1, 2, 13, 2),     # AlexNet conv2 geometry
     (True, 192, 96, 3, 1, 1, 13, 2),
     (True, 32, 48, 1, 1, 0, 9, 3),       # GEMM loader
-    (True, 384, 64, 3, 1, 1, 7, 2),      # K = 3456: six reduction slices (AlexNet conv4 shape)
-    (True, 512, 32, 3, 1, 1, 5, 2),      # K = 4608: eight slices
+    (True, 384, 64, 3, 1, 1, 7, 2),      # K = 3456: 13 reduction slices (AlexNet conv4 shape)
+    (True, 512, 32, 3, 1, 1, 5, 2),      # K = 4608: 16 slices (the cap)
 ]
 
 
