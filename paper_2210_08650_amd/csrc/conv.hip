@@ -1932,9 +1932,16 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
       return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
     } else if (a.N <= 128) {
       if (a.kh == 1 && a.K <= 256 && a.K >= 2 * BK) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
+      // 3 x 3 over 64 channels to 128 (VGG conv2_1): persistent 256 x 128
+      // tiles (VGG-16 b128 +1.6%)
+      if (a.kh == 3 && a.K <= 9 * 64 && a.K >= 2 * BK) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
       if (a.kh == 1 && a.K >= 512) return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
       if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
     } else if (a.N >= 512 && a.K >= 2048) {
+      // The longest reductions with enough rows: 128 x 256 tiles (VGG-16 b128
+      // conv4/conv5 and ResNet-50 b256 stage-4 3 x 3s: +2% and +0.6%; with
+      // fewer rows, ResNet-50 b128, 256 x 128 stays faster)
+      if (a.K >= 4096 && a.M >= 6272) return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
       return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
     } else if (a.K >= 2 * BK) {
       return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
