@@ -1935,7 +1935,13 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
       // 3 x 3 over 64 channels to 128 (VGG conv2_1): persistent 256 x 128
       // tiles (VGG-16 b128 +1.6%)
       if (a.kh == 3 && a.K <= 9 * 64 && a.K >= 2 * BK) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
-      if (a.kh == 1 && a.K >= 512) return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
+      // 1 x 1 with K >= 512 (ResNet-50 stage-2 reductions): with partitions
+      // in flight persistent 256 x 128 tiles (b256 +1.0%, b512 +0.8%), alone
+      // the latency-bound three-workgroups-per-CU tiles
+      if (a.kh == 1 && a.K >= 512) {
+        if (a.lanes >= 2) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
+        return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
+      }
       if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
     } else if (a.N >= 512 && a.K >= 2048) {
       // The longest reductions with enough rows: 128 x 256 tiles (VGG-16 b128
