@@ -1888,7 +1888,8 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
   //   channels and for 128-channel 3 x 3 layers; with three workgroups per CU
   //   (128 x 64 tiles, two stages: more loads in flight for these
   //   latency-bound layers) for residual layers with >= 1024 output channels
-  //   and 128-channel 1 x 1 layers with K >= 512;
+  //   and, with one partition in flight, 128-channel 1 x 1 layers with
+  //   K >= 512;
   // - the persistent kernel (one workgroup of 8 consumer and 4 producer waves
   //   per CU) with 128 x 256 tiles for the fused shortcut GEMMs and the other
   //   layers, and with 256 x 128 tiles for 128-channel 1 x 1 layers with short
