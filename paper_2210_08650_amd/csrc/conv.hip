@@ -1923,18 +1923,21 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
   if (LD == LD_GEMM && a.Kp == 2 * BK && a.N == 512 && a.res) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s);
   if (ws_eligible(a, (Loader)LD)) {
     if (LD == LD_S2D) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
-    // Long reductions whose 256-row tiles cannot fill the CUs, with no other
-    // partition in flight to fill them: persistent 128 x 128 tiles (twice the
-    // tiles; ResNet-18 b64 stage 3: 111 -> 82 us, ResNet-50 b32: 31.8k ->
-    // 37.4k images/s).  With two partitions in flight the larger tiles stay
-    // faster (ResNet-50 b256: 70.1k against 67.2k images/s).
-    // Fewer 128 x 128 tiles than half the CUs: 64 x 64 tiles, four stages
-    // (ResNet-50 b8: 706 -> 528 us of convolutions per pass; b32 stage 4:
-    // 3 x 3s 30 -> 20 us).
+    // With one partition in flight (none other fills the CUs this launch
+    // leaves idle):
+    // - fewer 128 x 128 tiles than half the CUs: 64 x 64 tiles, four stages
+    //   (ResNet-50 b8: 706 -> 528 us of convolutions per pass; b32 stage-4
+    //   3 x 3s 30 -> 20 us);
+    // - long reductions with fewer 256-row tiles than half the CUs:
+    //   persistent 128 x 128 tiles (ResNet-18 b64 stage 3: 111 -> 82 us,
+    //   ResNet-50 b32 31.8k -> 37.4k img/s).  With more (ResNet-50 stage 4 at
+    //   M = 12544: 196 tiles) 256 x 128 stays faster, 60 against 73 us, and
+    //   with two partitions in flight the larger tiles win throughout
+    //   (ResNet-50 b256: 70.1k against 67.2k img/s).
     if (a.lanes <= 1 && a.N >= 64 && 2 * (int64_t)((a.M + 127) / 128) * ((a.N + 127) / 128) < a.cus)
       return launch_ws_ld<64, 64, 2, 2, 4, LD, 0, 2>(a, s);
     if (a.lanes <= 1 && a.N >= 128 && a.K >= 1024 &&
-        (int64_t)((a.M + 255) / 256) * ((a.N + 127) / 128) < a.cus)
+        2 * (int64_t)((a.M + 255) / 256) * ((a.N + 127) / 128) < a.cus)
       return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 2>(a, s);
     // 32 output channels (DenseNet growth): a 32-column tile, so no MFMA
     // works on padding; 32 x 32 per consumer wave, three stages (DenseNet-121
@@ -1965,10 +1968,12 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
       }
       if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
     } else if (a.N >= 512 && a.K >= 2048) {
-      // The longest reductions with enough rows: 128 x 256 tiles (VGG-16 b128
-      // conv4/conv5 and ResNet-50 b256 stage-4 3 x 3s: +2% and +0.6%; with
-      // fewer rows, ResNet-50 b128, 256 x 128 stays faster)
-      if (a.K >= 4096 && a.M >= 6272) return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
+      // The longest reductions with enough rows, partitions in flight:
+      // 128 x 256 tiles (VGG-16 b128 conv4/conv5 and ResNet-50 b256 stage-4
+      // 3 x 3s: +2% and +0.6%); with fewer rows (ResNet-50 b128) or one
+      // partition (ResNet-50 stage 4 at M = 12544: 60 against 73 us),
+      // 256 x 128 stays faster.
+      if (a.K >= 4096 && a.M >= 6272 && a.lanes >= 2) return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
       return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
     } else if (a.K >= 2 * BK) {
       return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
