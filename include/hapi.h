@@ -4,9 +4,9 @@
  * The library runs the storage-side half of split transfer learning: the
  * forward pass of a frozen CNN or ViT feature extractor from the input images
  * up to a chosen split layer (paper: Design and Implementation, "Request
- * flow" -- the server executes feature extraction up to the split index; and
- * System implementation -- custom models that run the forward pass between
- * arbitrary layers), plus the per-layer output-size and forward-time profile
+ * flow", where the storage tier computes the frozen layers as far as the
+ * requested split and returns their output; and System implementation, whose
+ * models can run any contiguous range of layers), plus the per-layer output-size and forward-time profile
  * that split selection consumes (Design, "Profiling and modeling runtime" and
  * Table 1: output sizes from a batch-1 pass scale linearly with the batch;
  * the server-side forward pass is a profiled phase).
@@ -184,6 +184,18 @@ int hapi_layer_shape(const hapi_model_desc *desc, int32_t layer, int64_t *dims, 
 int64_t hapi_workspace_bytes(const hapi_model_desc *desc, int32_t batch, int32_t split_layer,
                              int32_t profile);
 
+/* Guard gaps of the workspace hapi_extract uses for (batch, split_layer)
+ * with desc->chunk and desc->inflight: each of the library's workspace
+ * regions (three activation slots and a partial-sum region per partition in
+ * flight) is followed by HAPI_GUARD_BYTES that no kernel writes.  Writes the
+ * byte offsets of the gaps, relative to desc->workspace, into
+ * offsets[0 .. min(count, max_entries)) and returns their count (0 for split
+ * 0), or a negative hapi_status.  For checking kernels' bounds: fill the gaps
+ * with a pattern before a call, compare them after it.  Host only. */
+#define HAPI_GUARD_BYTES 4096
+int32_t hapi_workspace_guards(const hapi_model_desc *desc, int32_t batch, int32_t split_layer,
+                              int64_t *offsets, int32_t max_entries);
+
 /* Number of partitions (storage-side batches) hapi_extract uses for `batch`
  * images with desc->chunk (Storage-side batch size adaptation: a request is
  * processed as partitions of the storage-side batch; the last partition may
@@ -238,6 +250,14 @@ int hapi_extract_range(const hapi_model_desc *desc, const void *weights, const v
  *                 synthetic weights and inputs written into the workspace
  *                 (out_us[0] = 0).  NULL skips timing; then the call touches
  *                 no device and works without a GPU.
+ * The partitions hapi_extract would use run one after another on
+ * desc->stream, each layer bracketed by events, with the tile choice
+ * hapi_extract makes for the same batch (which depends on the partitions it
+ * keeps in flight), so the kernels timed are the ones an extraction runs; the
+ * ResNet stem and its max pooling, fused in an extraction, are timed as the
+ * two layers they are.  With one partition in flight the sum over layers
+ * approximates an extraction's time; with several, it exceeds it by the
+ * overlap of the partitions.
  * Synchronous.  With out_us the workspace must hold
  * hapi_workspace_bytes(desc, batch, n_layers, 1) bytes. */
 int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out_bytes,

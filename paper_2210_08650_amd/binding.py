@@ -29,7 +29,7 @@ __all__ = ["HapiError", "Desc", "hapi_layer", "hapi_model_desc", "hapi_kernel_st
            "HAPI_BATCHNORM", "LIB_PATH", "EXPORTED",
            "hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
            "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-           "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
+           "hapi_workspace_guards", "HAPI_GUARD_BYTES", "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
            "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error", "hapi_split_job", "hapi_split_estimate", "hapi_split_choice", "hapi_choose_split"]
 
 _STATUS = {HAPI_E_INVAL: "HAPI_E_INVAL", HAPI_E_UNSUPPORTED: "HAPI_E_UNSUPPORTED",
@@ -125,6 +125,7 @@ def _load():
         "hapi_layer_shape": (ctypes.c_int, [D, i32, ctypes.POINTER(i64), ctypes.POINTER(i32)]),
         "hapi_workspace_bytes": (i64, [D, i32, i32, i32]),
         "hapi_chunk_count": (i32, [D, i32]),
+        "hapi_workspace_guards": (i32, [D, i32, i32, ctypes.POINTER(i64), i32]),
         "hapi_extract": (ctypes.c_int, [D, vp, vp, i32, i32, vp]),
         "hapi_extract_range": (ctypes.c_int, [D, vp, vp, i32, i32, i32, vp]),
         "hapi_profile_layers": (ctypes.c_int, [D, i32, ctypes.POINTER(i64),
@@ -146,7 +147,7 @@ def _load():
 _lib = _load()
 EXPORTED = ("hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
             "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-            "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
+            "hapi_workspace_guards", "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
             "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error", "hapi_choose_split")
 
 
@@ -196,6 +197,10 @@ class Desc:
         if stream is not None:
             self.c.stream = _stream(stream)
         if workspace is not None:
+            # Keep the owner alive while the descriptor points at its memory: a
+            # temporary tensor would otherwise return to torch's caching
+            # allocator and be reused under the library's feet.
+            self._workspace = workspace
             self.c.workspace = _ptr(workspace)
         if workspace_bytes is not None:
             self.c.workspace_bytes = int(workspace_bytes)
@@ -235,6 +240,18 @@ def hapi_layer_shape(desc: Desc, layer: int) -> tuple:
 
 def hapi_workspace_bytes(desc: Desc, batch: int, split_layer: int, profile: bool = False) -> int:
     return _check(_lib.hapi_workspace_bytes(desc.ref, int(batch), int(split_layer), int(profile)))
+
+
+HAPI_GUARD_BYTES = 4096
+
+
+def hapi_workspace_guards(desc: Desc, batch: int, split_layer: int) -> list:
+    """Byte offsets (relative to the workspace) of the HAPI_GUARD_BYTES gaps no
+    kernel writes."""
+    n = _check(_lib.hapi_workspace_guards(desc.ref, int(batch), int(split_layer), None, 0))
+    arr = (ctypes.c_int64 * max(n, 1))()
+    _check(_lib.hapi_workspace_guards(desc.ref, int(batch), int(split_layer), arr, n))
+    return [int(arr[i]) for i in range(n)]
 
 
 def hapi_chunk_count(desc: Desc, batch: int) -> int:

@@ -421,10 +421,34 @@ int64_t part_bytes(const Model &m, int split, int chunk) {
   return align_up((int64_t)chunk * max_part(m, split) * 4);
 }
 
-// Three activation slots and the partial-sum region per partition in flight
-// (profiling runs one).
+// Workspace of one partition in flight: three activation slots and the
+// partial-sum region, each followed by a guard gap of kGuardBytes that no
+// kernel writes (a write past a region's end lands in its gap, where a check
+// of the gap's contents sees it instead of it corrupting the next region).
+constexpr int64_t kGuardBytes = 4096;
+struct LaneLayout {
+  int64_t slot[3], part, bytes;
+  int64_t guard[4];
+};
+LaneLayout lane_layout(const Model &m, int split, int chunk) {
+  LaneLayout L;
+  const int64_t sb = slot_bytes(m, split, chunk);
+  int64_t o = 0;
+  for (int i = 0; i < 3; ++i) {
+    L.slot[i] = o;
+    L.guard[i] = o + sb;
+    o += sb + kGuardBytes;
+  }
+  L.part = o;
+  L.guard[3] = o + part_bytes(m, split, chunk);
+  L.bytes = L.guard[3] + kGuardBytes;
+  return L;
+}
+
+// One lane layout per partition in flight (profiling runs one), then for
+// profiling the synthetic packed weights and images.
 int64_t workspace_for(const Model &m, int split, int chunk, bool profile, int batch, int lanes) {
-  int64_t b = split > 0 ? (profile ? 1 : lanes) * (3 * slot_bytes(m, split, chunk) + part_bytes(m, split, chunk)) : 0;
+  int64_t b = split > 0 ? (profile ? 1 : lanes) * lane_layout(m, split, chunk).bytes : 0;
   if (profile) b += align_up(m.packed_bytes) + align_up((int64_t)batch * m.input.elems() * m.esz);
   return b;
 }
@@ -514,17 +538,11 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
                     const void *x2 = nullptr, const Act *in2 = nullptr, PreAct pre = PreAct{}) {
   ConvArgs a{};
   a.cus = c.cus;
-  {
-    // Every other convolution of a partition walks its tiles backwards, so
-    // it starts on the rows its producer wrote last, the ones most likely
-    // still in the last-level cache (ResNet-50 b256 +0.6%, ResNet-18 b64
-    // +1%; the order never changes a result).  HAPI_REV=0 turns it off.
-    static const int rv = [] {
-      const char *e = getenv("HAPI_REV");
-      return e ? atoi(e) : 1;
-    }();
-    a.rev = rv ? (c.seq++ & 1) : 0;
-  }
+  // Every other convolution of a partition walks its tiles backwards, so it
+  // starts on the rows its producer wrote last, the ones most likely still in
+  // the last-level cache (ResNet-50 b256 +0.6%, ResNet-18 b64 +1%; the order
+  // never changes a result).
+  a.rev = c.seq++ & 1;
   a.lanes = c.lanes;
   a.pre_scale = pre.scale;
   a.pre_shift = pre.shift;
@@ -971,13 +989,16 @@ int get_lanes(hipStream_t s, Lanes **out) {
 // partition p runs on lane p % lanes (lane 0 is desc->stream, the others
 // auxiliary streams forked from it and joined back into it at the end) with
 // that lane's three workspace slots.  Partitions are independent, and each
-// gives the same bits whichever lane runs it.
+// gives the same bits whichever lane runs it.  `route_lanes` is the number of
+// partitions in flight the kernels' tile choice assumes: `lanes` for an
+// extraction; for the per-layer profile, which runs the partitions one after
+// another, the number an extraction of the same batch would run, so that the
+// profile times the kernels the extraction runs.
 int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, const void *images,
               int batch, int start, int split, void *out, uint8_t *ws, int chunk, int lanes,
-              const std::function<void(int, bool)> &on_layer) {
+              int route_lanes, const std::function<void(int, bool)> &on_layer) {
   hipStream_t s = static_cast<hipStream_t>(d->stream);
-  const int64_t sb = slot_bytes(m, split, chunk);
-  const int64_t lane_bytes = 3 * sb + part_bytes(m, split, chunk);
+  const LaneLayout ll = lane_layout(m, split, chunk);
   Lanes *L = nullptr;
   if (lanes > 1) {
     if (int r = get_lanes(s, &L)) return r;
@@ -990,10 +1011,11 @@ int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, con
   // halving it per lane was measured slower (ResNet-50 b256: 69.5k -> 66k img/s).
   const int cus = cu_count();
   for (int i = 0; i < lanes; ++i) {
-    uint8_t *w0 = ws + (int64_t)i * lane_bytes;
+    uint8_t *w0 = ws + (int64_t)i * ll.bytes;
     c.push_back(Ctx{m, i ? L->aux[i - 1] : s, static_cast<const uint8_t *>(weights),
-                    {w0, w0 + sb, w0 + 2 * sb}, on_layer, cus, reinterpret_cast<float *>(w0 + 3 * sb),
-                    std::min(lanes, (batch + chunk - 1) / chunk)});
+                    {w0 + ll.slot[0], w0 + ll.slot[1], w0 + ll.slot[2]}, on_layer, cus,
+                    reinterpret_cast<float *>(w0 + ll.part),
+                    std::min(route_lanes, (batch + chunk - 1) / chunk)});
   }
   const int64_t in_bytes = act_at(m, start).elems() * m.esz;
   const int64_t out_bytes = m.layers[split - 1].out.elems() * m.esz;
@@ -1070,6 +1092,26 @@ int64_t hapi_workspace_bytes(const hapi_model_desc *desc, int32_t batch, int32_t
   return workspace_for(m, split_layer, chunk, profile != 0, batch, lanes_for(desc, chunk, batch));
 }
 
+int32_t hapi_workspace_guards(const hapi_model_desc *desc, int32_t batch, int32_t split_layer,
+                              int64_t *offsets, int32_t max_entries) {
+  Model m;
+  const int r = analyze(desc, m);
+  if (r != HAPI_OK) return r;
+  if (batch < 1) return fail(HAPI_E_INVAL, "batch must be >= 1");
+  if (split_layer < 0 || split_layer > (int)m.layers.size())
+    return fail(HAPI_E_INVAL, "split %d outside [0, %d]", split_layer, (int)m.layers.size());
+  if (max_entries < 0 || (max_entries > 0 && !offsets)) return fail(HAPI_E_INVAL, "offsets is NULL");
+  if (split_layer == 0) return 0;
+  const int chunk = chunk_for(desc, m, batch);
+  const int lanes = lanes_for(desc, chunk, batch);
+  const LaneLayout ll = lane_layout(m, split_layer, chunk);
+  int n = 0;
+  for (int l = 0; l < lanes; ++l)
+    for (int g = 0; g < 4; ++g, ++n)
+      if (n < max_entries) offsets[n] = (int64_t)l * ll.bytes + ll.guard[g];
+  return n;
+}
+
 int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void *packed) {
   Model m;
   int r = analyze(desc, m);
@@ -1143,7 +1185,7 @@ int extract_range(const hapi_model_desc *desc, const void *weights, const void *
                 (long long)need);
   if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
   return run_batch(desc, m, weights, images, batch, start_layer, split_layer, out,
-                   static_cast<uint8_t *>(desc->workspace), chunk, lanes, nullptr);
+                   static_cast<uint8_t *>(desc->workspace), chunk, lanes, lanes, nullptr);
 }
 
 }  // namespace
@@ -1203,8 +1245,7 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
   if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(desc->stream);
   uint8_t *ws = static_cast<uint8_t *>(desc->workspace);
-  const int64_t slots = 3 * slot_bytes(m, n, chunk) + part_bytes(m, n, chunk);
-  uint8_t *pk = ws + slots;
+  uint8_t *pk = ws + lane_layout(m, n, chunk).bytes;
   uint8_t *img = pk + align_up(m.packed_bytes);
   // Synthetic model and inputs: small pseudo-random values in every parameter.
   for (const LayerPlan &lp : m.layers) {
@@ -1225,6 +1266,9 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
   std::vector<float> acc(n);
   const int nchunks = (batch + chunk - 1) / chunk;
   const int per_pass = 2 * n * nchunks;
+  // Partitions run one after another on desc->stream (each layer is timed
+  // alone), with the tile choice of an extraction of this batch.
+  const int route = lanes_for(desc, chunk, batch);
   ev.resize(per_pass);
   for (auto &e : ev) HIP_TRY(hipEventCreate(&e));
   int rc = HAPI_OK;
@@ -1235,7 +1279,7 @@ int hapi_profile_layers(const hapi_model_desc *desc, int32_t batch, int64_t *out
       (void)begin;
       (void)hipEventRecord(ev[idx++], s);
     };
-    rc = run_batch(desc, m, pk, img, batch, 0, n, nullptr, ws, chunk, 1, cb);
+    rc = run_batch(desc, m, pk, img, batch, 0, n, nullptr, ws, chunk, 1, route, cb);
     if (rc != HAPI_OK) break;
     if (hipEventSynchronize(ev[idx - 1]) != hipSuccess) {
       rc = fail(HAPI_E_DEVICE, "hipEventSynchronize failed");

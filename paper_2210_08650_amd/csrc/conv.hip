@@ -16,9 +16,6 @@
 // of M.  Results are therefore bit-identical for any batch split.
 #include <cstdio>
 #include <cstdlib>
-#include <cstring>
-#include <vector>
-
 #include <type_traits>
 #include <utility>
 
@@ -709,20 +706,6 @@ __device__ __forceinline__ void dma16(const void *base, uint16_t *lds, unsigned 
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7fffffff, 0x00020000), LDS_PTR(lds), 16,
       voff, soff, 0, 0);
 }
-
-// As dma16, with an explicit buffer range in bytes.
-__device__ __forceinline__ void dma16_range(const void *base, uint16_t *lds, unsigned voff, unsigned soff,
-                                            unsigned range) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, range, 0x00020000), LDS_PTR(lds), 16, voff,
-      soff, 0, 0);
-}
-
-// Weight row moved by `lane` in row-group g (tile column 0).
-__device__ __forceinline__ int n0_zero(int g, int lane) { return g * 8 + (lane >> 3); }
-
-// Persistent workgroups of the streaming kernel: one per CU.
-constexpr int kStreamWorkgroups = 256;
 
 // Per-lane offsets of one producer lane.  Row-group g = ga + i (A) or gb + j
 // (B) covers rows 8 g .. 8 g + 7; lane l moves row 8 g + l / 8 and logical
@@ -1592,205 +1575,6 @@ hipError_t launch_pws_ld(const ConvArgs &a, hipStream_t s) {
   return launch_pws_cfg<BM, BN, WM, WN, PW, STAGES, LD, 1, EP>(a, s);
 }
 
-// ------------------------------------------- bf16, streaming 1 x 1 kernel
-//
-// For 1 x 1 convolutions with short K (the memory-bound ResNet layers) the
-// whole weight matrix [N][K] stays in LDS and persistent workgroups stream
-// BM-row tiles of the activations through a STAGES-deep ring: producer waves
-// (scalar instructions and buffer loads only, as above) run ahead across tile
-// boundaries while the consumer waves finish the previous tile's epilogue
-// straight from registers.  The activation rows of a tile are a contiguous
-// byte range, so each tile only moves the buffer base; rows beyond M fall
-// outside the buffer's range and read zeros.
-template <int BM, int BN, int WM, int WN, int STAGES, int LD>
-__global__ __launch_bounds__(2 * WM * WN * 64) void conv_bf16_stream_kernel(ConvArgs a) {
-  constexpr int CW = WM * WN;
-  constexpr int TM = BM / (WM * 32), TN = BN / (WN * 32);
-  constexpr int NA = BM / (8 * CW), NB = BN / (8 * CW);
-  constexpr int KS = BK / 16;
-  constexpr int kBRes = 65536;                 // bytes of LDS for the resident weights
-  constexpr int kStage = BM * BK;              // elements per activation stage
-  constexpr int kCR = TM * 32, kCC = TN * 32;  // a consumer wave's output block
-  constexpr int kCP = kCC + 4;                 // fp32 pitch of its staging rows
-  constexpr int kCBytes = CW * kCR * kCP * 4;
-  static_assert(NA * 8 * CW == BM && NB * 8 * CW == BN && TM >= 1 && TN >= 1, "tile");
-  static_assert(STAGES >= 2 && (STAGES - 2) * NA < 64, "stages");
-  static_assert(kBRes + STAGES * kStage * 2 + kCBytes <= 163840, "LDS");
-  __shared__ __attribute__((aligned(16))) uint8_t smem_raw[kBRes + STAGES * kStage * 2 + kCBytes];
-  uint16_t *bres = reinterpret_cast<uint16_t *>(smem_raw);
-  uint16_t *astage = reinterpret_cast<uint16_t *>(smem_raw + kBRes);
-  float *cstage = reinterpret_cast<float *>(smem_raw + kBRes + STAGES * kStage * 2);
-
-  const int t = threadIdx.x, lane = t & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const bool producer = wave >= CW;
-  const int nk = a.Kp / BK;
-  const int k1 = LD == LD_CAT ? a.K1 / BK : nk;  // k-tiles read from x (the rest from x2)
-  const int tiles = (a.M + BM - 1) / BM;
-  const int my_tiles = tiles > (int)blockIdx.x ? (tiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
-
-  if (producer) {
-    const int pw = wave - CW;
-    const int kcA = ((lane & 7) ^ ((lane >> 4) & 7)) * 8, kcB = ((lane & 7) ^ ((4 + (lane >> 4)) & 7)) * 8;
-    // per-lane byte offsets for the tile at row 0 (rows of x: K1 or K wide;
-    // rows of x2: C2 wide)
-    const int lda = LD == LD_CAT ? a.K1 : a.K;
-    unsigned va[NA], va2[LD == LD_CAT ? NA : 1];
-#pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const int r = (pw * NA + i) * 8 + (lane >> 3), kc8 = ((pw * NA + i) & 1) ? kcB : kcA;
-      va[i] = (unsigned)((r * lda + kc8) * 2);
-      if (LD == LD_CAT) va2[LD == LD_CAT ? i : 0] = (unsigned)((r * a.C2 + kc8) * 2);
-    }
-    // resident weights: k-tile kt of row-group g at bres + (kt * BN + 8 g) * 64
-    for (int kt = 0; kt < nk; ++kt) {
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int g = pw * NB + j, n = n0_zero(g, lane);
-        const unsigned vb = n < a.N ? (unsigned)((n * a.Kp + ((g & 1) ? kcB : kcA)) * 2) : kOob;
-        dma16(a.w, bres + (kt * BN + g * 8) * BK, vb, (unsigned)(kt * BK * 2));
-      }
-    }
-    const char *x = static_cast<const char *>(a.x), *x2 = static_cast<const char *>(a.x2);
-    const int64_t xbytes = (int64_t)a.M * lda * 2, x2bytes = LD == LD_CAT ? (int64_t)a.M * a.C2 * 2 : 0;
-    int q = 0;
-    for (int it = 0; it < my_tiles; ++it) {
-      const int64_t m0 = (int64_t)((int)blockIdx.x + it * (int)gridDim.x) * BM;
-      for (int kt = 0; kt < nk; ++kt) {
-        if (q >= STAGES - 1) {
-          wait_vmcnt<(STAGES - 2) * NA>();
-          __builtin_amdgcn_s_barrier();
-        }
-        uint16_t *As = astage + (q % STAGES) * kStage;
-        const bool second = LD == LD_CAT && kt >= k1;
-        const char *base = second ? x2 + m0 * a.C2 * 2 : x + m0 * lda * 2;
-        const int64_t left = second ? x2bytes - m0 * a.C2 * 2 : xbytes - m0 * lda * 2;
-        const unsigned range = (unsigned)(left < 0x7fffffff ? left : 0x7fffffff);
-        const unsigned so = (unsigned)((second ? kt - k1 : kt) * BK * 2);
-#pragma unroll
-        for (int i = 0; i < NA; ++i)
-          dma16_range(base, As + (pw * NA + i) * 512, second ? va2[LD == LD_CAT ? i : 0] : va[i], so, range);
-        ++q;
-      }
-    }
-    const int total = my_tiles * nk;
-    for (int b = max(0, total - STAGES + 1); b < total; ++b) {
-      const int younger = total - 1 - b;
-      if (STAGES >= 4 && younger >= 2) {
-        if (younger >= 3 && STAGES >= 5) wait_vmcnt<(STAGES >= 5 ? 3 : 0) * NA>();
-        else wait_vmcnt<(STAGES >= 4 ? 2 : 0) * NA>();
-      } else if (STAGES >= 3 && younger >= 1) wait_vmcnt<(STAGES >= 3 ? 1 : 0) * NA>();
-      else wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
-    }
-    return;
-  }
-
-  const int wm = wave / WN, wn = wave % WN;
-  const int lrow = lane & 31, lh = lane >> 5;
-  const int sw = (lrow >> 1) & 7;
-  int aoff[TM], boff[TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) aoff[i] = (wm * TM * 32 + i * 32 + lrow) * BK;
-#pragma unroll
-  for (int j = 0; j < TN; ++j) boff[j] = (wn * TN * 32 + j * 32 + lrow) * BK;
-  uint16_t *y = static_cast<uint16_t *>(a.y);
-  const uint16_t *res = static_cast<const uint16_t *>(a.res);
-  int q = 0;
-  for (int it = 0; it < my_tiles; ++it) {
-    const int m0 = ((int)blockIdx.x + it * (int)gridDim.x) * BM;
-    f32x16_t acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-    for (int kt = 0; kt < nk; ++kt, ++q) {
-      __builtin_amdgcn_s_barrier();
-      const uint16_t *S = astage + (q % STAGES) * kStage;
-      const uint16_t *Bk = bres + kt * BN * BK;
-      bf16x8_t af[2][TM], bfr[2][TN];
-      auto read_frags = [&](int ks, int buf) {
-        const int ch = ((2 * ks + lh) ^ sw) * 8;
-#pragma unroll
-        for (int i = 0; i < TM; ++i) af[buf][i] = *reinterpret_cast<const bf16x8_t *>(S + aoff[i] + ch);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) bfr[buf][j] = *reinterpret_cast<const bf16x8_t *>(Bk + boff[j] + ch);
-      };
-      read_frags(0, 0);
-      static_for<KS>([&](auto ksc) {
-        constexpr int ks = decltype(ksc)::value;
-        constexpr int cur = ks & 1;
-        if constexpr (ks + 1 < KS) read_frags(ks + 1, cur ^ 1);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
-      });
-    }
-    // Epilogue, per wave: acc + bias goes to the wave's own LDS block (lane
-    // holds C[row][col .. col + 3], row = 32 i + lane % 32, col = 32 j + 8 g +
-    // 4 (lane / 32)); then each lane finishes 8 consecutive channels of a row
-    // (residual, activation, one rounding) and stores 16 bytes, so a store
-    // instruction writes whole rows of the block.
-    float *Cw = cstage + wave * kCR * kCP;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int col = j * 32 + 8 * g + 4 * lh;
-        const int n = wn * kCC + col;
-        const float4 bv = a.bias ? *reinterpret_cast<const float4 *>(a.bias + n) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          *reinterpret_cast<float4 *>(Cw + (i * 32 + lrow) * kCP + col) =
-              make_float4(acc[i][j][4 * g] + bv.x, acc[i][j][4 * g + 1] + bv.y, acc[i][j][4 * g + 2] + bv.z,
-                          acc[i][j][4 * g + 3] + bv.w);
-      }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    constexpr int CPR = kCC / 8;  // 8-channel chunks per block row
-#pragma unroll 4
-    for (int c = lane; c < kCR * CPR; c += 64) {
-      const int row = c / CPR, col = (c % CPR) * 8;
-      const int m = m0 + wm * kCR + row, n = wn * kCC + col;
-      const float4 p = *reinterpret_cast<const float4 *>(Cw + row * kCP + col);
-      const float4 q2 = *reinterpret_cast<const float4 *>(Cw + row * kCP + col + 4);
-      if (m >= a.M) continue;
-      float v[8] = {p.x, p.y, p.z, p.w, q2.x, q2.y, q2.z, q2.w};
-      if (res) {
-        const uint4 rv = *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n);
-        const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[2 * e] += bf2f((uint16_t)(w4[e] & 0xffff));
-          v[2 * e + 1] += bf2f((uint16_t)(w4[e] >> 16));
-        }
-      }
-      uint32_t o[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        o[e] = f2bf2(epilogue_act(v[2 * e], a.relu, a.gelu), epilogue_act(v[2 * e + 1], a.relu, a.gelu));
-      *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  }
-}
-
-template <int BM, int BN, int WM, int WN, int STAGES, int LD>
-hipError_t launch_stream_cfg(const ConvArgs &a, hipStream_t s) {
-  const int tiles = (a.M + BM - 1) / BM;
-  const int grid = tiles < kStreamWorkgroups ? tiles : kStreamWorkgroups;
-  hapi_launch((conv_bf16_stream_kernel<BM, BN, WM, WN, STAGES, LD>), dim3(grid), dim3(2 * WM * WN * 64), 0,
-                     s, a);
-  return hipGetLastError();
-}
-
 // Whether the warp-specialised kernel handles this launch: whole 64-wide
 // k-tiles, kernel taps it was built for, and every operand addressable with
 // 31-bit byte offsets.
@@ -1822,84 +1606,10 @@ hipError_t launch_ws_ld(const ConvArgs &a, hipStream_t s) {
   return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, 1, EPI, MINB>(a, s);
 }
 
-// Tuning override: HAPI_CONV_CFG=<index> forces one tile configuration.
-int forced_cfg() {
-  static const int v = [] {
-    const char *e = getenv("HAPI_CONV_CFG");
-    return e ? atoi(e) : -1;
-  }();
-  return v;
-}
-
-// Tuning override per shape: HAPI_CFG_FOR="N:K:index,..." forces a tile
-// configuration on the layers with N outputs and reduction length K.
-int shape_cfg(const ConvArgs &a) {
-  struct Rule { int n, k, cfg; };
-  static const std::vector<Rule> rules = [] {
-    std::vector<Rule> r;
-    const char *e = getenv("HAPI_CFG_FOR");
-    while (e && *e) {
-      Rule x{};
-      if (sscanf(e, "%d:%d:%d", &x.n, &x.k, &x.cfg) == 3) r.push_back(x);
-      e = strchr(e, ',');
-      if (e) ++e;
-    }
-    return r;
-  }();
-  for (const Rule &x : rules)
-    if (x.n == a.N && x.k == a.K) return x.cfg;
-  return -1;
-}
-
 // Tile shape per layer.  Every shape uses the same k-tile and MFMA, so the
 // choice never changes a result bit.
 template <int LD>
 hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
-  const int fc = forced_cfg() >= 0 ? forced_cfg() : shape_cfg(a);
-  if (fc >= 20 && !ws_eligible(a, (Loader)LD)) return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);
-  switch (fc) {
-    case 0: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 0>(a, s);
-    case 1: return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1, 0>(a, s);
-    case 2: return launch_pipe_cfg<128, 128, 2, 2, 2, LD, 1, 1>(a, s);
-    case 3: return launch_pipe_cfg<128, 64, 2, 2, 3, LD, 1, 1>(a, s);
-    case 4: return launch_pipe_cfg<128, 64, 2, 2, 2, LD, 1, 1>(a, s);
-    case 5: return launch_pipe_cfg<256, 128, 4, 2, 2, LD, 1, 1>(a, s);
-    case 6: return launch_pipe_cfg<256, 256, 4, 2, 2, LD, 1, 1>(a, s);
-    case 7: return launch_pipe_cfg<128, 256, 2, 4, 2, LD, 1, 1>(a, s);
-    case 8: return launch_pipe_cfg<256, 128, 2, 2, 2, LD, 1, 1>(a, s);
-    case 9: return launch_pipe_cfg<128, 128, 2, 2, 3, LD, 1, 1>(a, s);
-    case 10: return launch_pipe_cfg<256, 64, 4, 1, 2, LD, 1, 1>(a, s);
-    case 11: return launch_pipe_cfg<64, 128, 1, 4, 3, LD, 1, 1>(a, s);
-    case 12: return launch_pipe_cfg<256, 256, 2, 2, 2, LD, 1, 1>(a, s);
-    case 20: return launch_ws_ld<256, 128, 2, 2, 3, LD, 0, 1>(a, s);
-    case 21: return launch_ws_ld<128, 128, 2, 2, 4, LD, 0, 1>(a, s);
-    case 22: return launch_ws_ld<128, 256, 2, 2, 3, LD, 0, 1>(a, s);
-    case 23: return launch_ws_ld<256, 64, 4, 1, 4, LD, 0, 1>(a, s);
-    case 24: return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
-    case 25: return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
-    case 40: return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 1>(a, s);
-    case 41: return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
-    case 42: return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
-    case 43: return launch_pws_ld<256, 128, 4, 2, 2, 3, LD, 2>(a, s);
-    case 44: return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 2>(a, s);
-    case 45: return launch_pws_ld<256, 64, 4, 1, 4, 3, LD, 2>(a, s);
-    case 46: return launch_pws_ld<256, 64, 8, 1, 4, 3, LD, 2>(a, s);
-    case 47: return launch_pws_ld<256, 128, 4, 2, 4, 2, LD, 2>(a, s);
-    case 57: return launch_ws_ld<256, 32, 4, 1, 2, LD, 0, 2>(a, s);
-    case 58: return launch_ws_ld<64, 64, 2, 2, 4, LD, 0, 2>(a, s);
-    case 59: return launch_ws_ld<64, 64, 2, 2, 3, LD, 0, 3>(a, s);
-    case 60: return launch_ws_ld<64, 128, 2, 2, 3, LD, 0, 2>(a, s);
-    case 61: return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
-    case 62: return launch_ws_ld<128, 32, 4, 1, 2, LD, 0, 2>(a, s);
-    case 63: return launch_ws_ld<128, 32, 4, 1, 2, LD, 0, 3>(a, s);
-    case 64: return launch_ws_ld<128, 32, 4, 1, 3, LD, 0, 2>(a, s);
-    case 50: if (a.Kp <= 2 * BK) return launch_short_ld<128, 128, 2, 2, LD, 3>(a, s); break;
-    case 51: if (a.Kp <= 2 * BK) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s); break;
-    case 52: if (a.Kp <= 2 * BK) return launch_short_ld<64, 128, 2, 2, LD, 4>(a, s); break;
-    case 53: if (a.Kp <= 2 * BK) return launch_short_ld<128, 256, 2, 4, LD, 2>(a, s); break;
-    case 54: if (a.Kp <= 2 * BK) return launch_short_ld<64, 64, 2, 2, LD, 4>(a, s); break;
-    default: break;
-  }
   // Measured on MI355X over the ResNet-50 conv shapes (per-layer kernel
   // traces of every configuration above):
   // - the warp-specialised kernel with two workgroups per CU (128 x 64 tiles)
@@ -2208,35 +1918,6 @@ hipError_t launch_f32_cfg(const ConvArgs &a, hipStream_t s) {
 
 }  // namespace
 
-// Streaming kernel: 1 x 1 stride-1 convolutions (a shortcut part, if any, also
-// 1 x 1 stride 1) whose whole weight matrix fits the 64 KB resident region.
-// Measured slower than the tiled kernels on the ResNet-50 layer-1 shapes (its
-// LDS holds too few activation stages next to the resident weights and the
-// output staging to cover the load latency), so it runs only on request
-// (HAPI_CONV_CFG=30).
-hipError_t launch_stream(const ConvArgs &a, Loader ld, hipStream_t s) {
-  if (forced_cfg() != 30) return hipErrorNotSupported;
-  if (ld != LD_GEMM && ld != LD_CAT) return hipErrorNotSupported;
-  if (a.K % BK != 0 || (int64_t)a.N * a.Kp * 2 > 65536 || a.ldc % 8 != 0 || a.ldr % 8 != 0)
-    return hipErrorNotSupported;
-  if (ld == LD_CAT && (a.kh != 1 || a.stride != 1 || a.s2 != 1 || a.K1 % BK != 0 || a.C2 % BK != 0))
-    return hipErrorNotSupported;
-  const int64_t lim = (int64_t)1 << 31;
-  if ((int64_t)a.M * a.K * 2 >= lim) return hipErrorNotSupported;
-  switch (a.N) {
-    case 64:
-      return ld == LD_GEMM ? launch_stream_cfg<128, 64, 2, 2, 3, LD_GEMM>(a, s)
-                           : launch_stream_cfg<128, 64, 2, 2, 3, LD_CAT>(a, s);
-    case 128:
-      return ld == LD_GEMM ? launch_stream_cfg<64, 128, 2, 2, 4, LD_GEMM>(a, s)
-                           : launch_stream_cfg<64, 128, 2, 2, 4, LD_CAT>(a, s);
-    case 256:
-      return ld == LD_GEMM ? launch_stream_cfg<64, 256, 1, 4, 3, LD_GEMM>(a, s)
-                           : launch_stream_cfg<64, 256, 1, 4, 3, LD_CAT>(a, s);
-    default: return hipErrorNotSupported;
-  }
-}
-
 hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
   if (a.pre_scale || (a.lda && a.lda != a.K)) {
     // Pre-activated or strided A (a channel prefix of a wider tensor): the
@@ -2259,13 +1940,11 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
     }
     return launch_pipe_cfg<128, 128, 2, 2, 2, LD_GEMM, 1, 0, true>(a, s);
   }
-  if (launch_stream(a, ld, s) == hipSuccess) return hipSuccess;
   switch (ld) {
     // The pipelined kernel needs 16-byte output rows; the register-staged one
     // handles element gathers (NCHW stems) and any other width.
     case LD_NHWC:
-      if (!a.gelu && a.Ho == a.H && a.Wo == a.W && forced_cfg() < 0 &&
-          conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
+      if (!a.gelu && a.Ho == a.H && a.Wo == a.W && conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
         return launch_conv3x3_c64(a.x, a.w, a.Kp, a.bias, a.res, a.ldr, a.y, a.ldc, a.n_img, a.H, a.W, a.relu != 0,
                                   a.cus > 0 ? a.cus : cu_count(), s);
       return (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) ? launch_pipe_ld<LD_NHWC>(a, s)
@@ -2284,7 +1963,7 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
       if (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) return launch_pipe_ld<LD_CAT>(a, s);
       break;
     case LD_NHWC8:
-      if (forced_cfg() < 0 && conv_first_supported(a)) return launch_conv_first(a, s);
+      if (conv_first_supported(a)) return launch_conv_first(a, s);
       if (a.N % 8 != 0 || a.ldc % 8 != 0 || a.ldr % 8 != 0 || !ws_eligible(a, LD_NHWC8)) break;
       if (a.N <= 64) return launch_ws_cfg<128, 64, 2, 2, 3, LD_NHWC8, 1, 0, 2>(a, s);
       return launch_ws_cfg<128, 128, 2, 2, 2, LD_NHWC8, 1, 0, 2>(a, s);

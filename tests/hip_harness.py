@@ -34,6 +34,35 @@ def images_for(dtype: int, imgs_f32: np.ndarray):
     return t.cuda(), imgs_f32.astype(np.float32)
 
 
+GUARD = 4096        # bytes of sentinel before and after every output and workspace
+SENTINEL = 0xA5     # byte pattern of the sentinel
+
+
+class Guarded:
+    """A device buffer with GUARD bytes of sentinel on both sides, plus the
+    library's own guard gaps inside a workspace; check() fails if a kernel
+    wrote into any of them."""
+
+    def __init__(self, nbytes, inner_gaps=()):
+        self.nbytes = int(nbytes)
+        self.raw = torch.full((self.nbytes + 2 * GUARD + 256,), SENTINEL, dtype=torch.uint8, device="cuda")
+        off = (-self.raw.data_ptr()) % 256 + GUARD     # 256-byte aligned body
+        self.off = off
+        self.body = self.raw[off:off + self.nbytes]
+        self.gaps = [(0, off), (off + self.nbytes, self.raw.numel())] + \
+                    [(off + g, off + g + H.HAPI_GUARD_BYTES) for g in inner_gaps]
+
+    def view(self, dtype, shape):
+        return self.body.view(dtype).view(shape)
+
+    def check(self):
+        for a, b in self.gaps:
+            seg = self.raw[a:b]
+            bad = int((seg != SENTINEL).sum())
+            assert bad == 0, f"{bad} bytes written into the guard [{a - self.off}, {b - self.off}) " \
+                             f"of a {self.nbytes}-byte buffer"
+
+
 class Runner:
     """A packed model resident on the GPU, ready for repeated extraction."""
 
@@ -54,29 +83,37 @@ class Runner:
     def out_shape(self, split):
         return H.hapi_layer_shape(self.desc, split)
 
-    def extract(self, images_dev, split, chunk=0, workspace_pad=0, out=None, inflight=0):
-        batch = images_dev.shape[0]
+    def _buffers(self, batch, split, chunk, inflight, workspace_pad=0):
+        """Guarded workspace and output: every call checks that no kernel
+        wrote outside its output, its workspace regions or its workspace."""
         self.desc.set(chunk=chunk, inflight=inflight)
         need = H.hapi_workspace_bytes(self.desc, batch, split)
-        ws = torch.empty(max(need + workspace_pad, 256), dtype=torch.uint8, device="cuda")
-        self.desc.set(workspace=ws, workspace_bytes=need + workspace_pad)
-        if out is None:
-            out = torch.empty((batch,) + self.out_shape(split), dtype=self.tdtype, device="cuda")
-        H.hapi_extract(self.desc, self.packed, images_dev, batch, split, out)
+        ws = Guarded(max(need + workspace_pad, 256), H.hapi_workspace_guards(self.desc, batch, split))
+        self.desc.set(workspace=ws.body, workspace_bytes=need + workspace_pad)
+        shape = (batch,) + self.out_shape(split)
+        out = Guarded(int(np.prod(shape)) * (2 if self.tdtype == torch.bfloat16 else 4))
+        return ws, out, out.view(self.tdtype, shape)
+
+    def extract(self, images_dev, split, chunk=0, workspace_pad=0, out=None, inflight=0):
+        batch = images_dev.shape[0]
+        ws, gout, o = self._buffers(batch, split, chunk, inflight, workspace_pad)
+        H.hapi_extract(self.desc, self.packed, images_dev, batch, split, o if out is None else out)
         torch.cuda.synchronize()
-        return out
+        ws.check()
+        if out is not None:
+            return out
+        gout.check()
+        return o.clone()
 
     def resume(self, input_dev, start, end, chunk=0, inflight=0):
         """Layers start+1..end on the layer-``start`` tensor (caller layout)."""
         batch = input_dev.shape[0]
-        self.desc.set(chunk=chunk, inflight=inflight)
-        need = H.hapi_workspace_bytes(self.desc, batch, end)
-        ws = torch.empty(max(need, 256), dtype=torch.uint8, device="cuda")
-        self.desc.set(workspace=ws, workspace_bytes=need)
-        out = torch.empty((batch,) + self.out_shape(end), dtype=self.tdtype, device="cuda")
-        H.hapi_extract_range(self.desc, self.packed, input_dev, batch, start, end, out)
+        ws, gout, o = self._buffers(batch, end, chunk, inflight)
+        H.hapi_extract_range(self.desc, self.packed, input_dev, batch, start, end, o)
         torch.cuda.synchronize()
-        return out
+        ws.check()
+        gout.check()
+        return o.clone()
 
     def extract_np(self, images_dev, split, chunk=0, inflight=0):
         return self.extract(images_dev, split, chunk, inflight=inflight).float().cpu().numpy()

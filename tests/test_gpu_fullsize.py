@@ -16,10 +16,12 @@ from tests.hip_harness import Runner, images_for, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-SAMPLES = {"alexnet_f32_b4": [0, 1, 2, 3], "resnet18_bf16_b64": [0, 17, 63],
-           "vgg16_bf16_b128": [0, 127], "resnet50_bf16_b256": [0, 97, 255],
-           "vit_b16_bf16_b128": [0, 64, 127], "densenet_block_bf16_b64": [0, 31, 63],
-           "densenet121_bf16_b256": [0, 255]}
+def samples(batch, n=8):
+    """n images spread over the batch, always the first and the last (every
+    image when the batch has at most n)."""
+    if batch <= n:
+        return list(range(batch))
+    return sorted({round(i * (batch - 1) / (n - 1)) for i in range(n)})
 
 
 @pytest.mark.parametrize("wl", list(PM.WORKLOADS))
@@ -34,11 +36,11 @@ def test_workload_full_batch_sampled(wl):
     assert got.shape == (cfg["batch"],) + om.shapes()[cfg["split"]]
     assert np.isfinite(got).all()
     tol = 1e-4 if cfg["dtype"] == H.HAPI_F32 else 2e-2
-    idx = SAMPLES[wl]
+    idx = samples(cfg["batch"])
     ref = om.forward(ps, xv[idx], cfg["split"])
     for j, i in enumerate(idx):
         err = rel_l2(got[i], ref[j])
-        print(f"{wl} image {i}: rel_l2 {err:.3e}", flush=True)
+        print(f"PARITY {wl} split {cfg['split']} image {i}: rel_l2 {err:.3e}", flush=True)
         assert err <= tol
     # run-to-run determinism and partition independence, bit for bit
     again = r.extract_np(xd, cfg["split"], chunk=max(1, cfg["batch"] // 3 + 1))
@@ -61,7 +63,32 @@ def test_resnet50_batch_512_two_full_partitions():
     ref = om.forward(ps, xv[idx], 18)
     for j, i in enumerate(idx):
         err = rel_l2(got[i], ref[j])
-        print(f"resnet50 b512 image {i}: rel_l2 {err:.3e}", flush=True)
+        print(f"PARITY resnet50_bf16_b512 split 18 image {i}: rel_l2 {err:.3e}", flush=True)
         assert err <= 2e-2
     # image 0 of a batch of 256 is computed by the same kernels with other partners
     assert np.array_equal(r.extract_np(xd[:256].contiguous(), 18), got[:256])
+
+
+@pytest.mark.parametrize("batch", [8, 32, 128])
+def test_resnet50_sweep_sampled(batch):
+    """The rest of the ResNet-50 batch sweep, each batch in the benchmark's
+    launch configuration (automatic partitions; tile choice depends on the
+    rows of each layer and on the partitions in flight: one at 8 and 32, two
+    64-image partitions at 128), against the oracle on images 0, B/2 and B-1.
+    Storage-side batch adaptation must not change the result, so image 0 also
+    equals its value in a batch of 256 bit for bit."""
+    cfg = PM.WORKLOADS["resnet50_bf16_b256"]
+    om = OM.build("resnet50")
+    ps = synth.params(cfg["seed"], om.manifest())
+    imgs = synth.images(cfg["seed"], 256)
+    xd, xv = images_for(H.HAPI_BF16, imgs)
+    r = Runner(PM.resnet50(), H.HAPI_BF16, ps)
+    got = r.extract_np(xd[:batch].contiguous(), 18)
+    idx = [0, batch // 2, batch - 1]
+    ref = om.forward(ps, xv[idx], 18)
+    for j, i in enumerate(idx):
+        err = rel_l2(got[i], ref[j])
+        print(f"PARITY resnet50_bf16_b{batch} split 18 image {i}: rel_l2 {err:.3e}", flush=True)
+        assert err <= 2e-2
+    full = r.extract_np(xd, 18)
+    assert np.array_equal(full[:batch], got)

@@ -40,7 +40,7 @@ def test_every_split_matches_oracle(name, batch):
     for split in range(0, om.n_layers + 1):
         got = r.extract_np(xd, split)
         err = rel_l2(got, outs[split])
-        print(f"{name} split {split}: rel_l2 {err:.3e}", flush=True)
+        print(f"PARITY {name}_b{batch} split {split}: rel_l2 {err:.3e}", flush=True)
         assert got.shape == outs[split].shape
         if split == 0:
             assert np.array_equal(got, xv)
@@ -161,6 +161,44 @@ def test_profile_layers_times_every_layer():
     b, us = H.hapi_profile_layers(d, 32, True)
     assert us[0] == 0.0 and all(t > 0 for t in us[1:]), us
     assert b == H.hapi_profile_layers(d, 32)[0]
+
+
+@pytest.mark.parametrize("batch,chunk,inflight", [(32, 0, 1), (64, 16, 1), (256, 0, 0)])
+def test_profile_time_matches_extraction(batch, chunk, inflight):
+    """The per-layer times the split choice consumes add up to the time of an
+    extraction of the same batch: within [0.8, 1.5] of it with one partition
+    in flight (the profile times the stem and its pooling unfused and adds an
+    event pair per layer; the extraction adds the split's layout pass), and
+    with two partitions in flight (256 images) between 0.9 and 2.5 times it,
+    since the profile runs the partitions one after another."""
+    d = H.Desc(PM.resnet50(), H.HAPI_BF16, stream=torch.cuda.current_stream(), chunk=chunk,
+               inflight=inflight)
+    need = H.hapi_workspace_bytes(d, batch, 18, True)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    d.set(workspace=ws, workspace_bytes=need)
+    _, us = H.hapi_profile_layers(d, batch, True)
+    prof_ms = sum(us[1:19]) / 1e3
+    r, _, _, xd, _, _ = _setup("resnet50", 73, batch)
+    r.extract(xd, 18, chunk=chunk, inflight=inflight)  # warm
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ts = []
+    for _ in range(7):
+        need = H.hapi_workspace_bytes(r.desc.set(chunk=chunk, inflight=inflight), batch, 18)
+        w2 = torch.empty(need, dtype=torch.uint8, device="cuda")
+        out = torch.empty((batch, 2048, 7, 7), dtype=torch.bfloat16, device="cuda")
+        r.desc.set(workspace=w2, workspace_bytes=need)
+        torch.cuda.synchronize()
+        ev[0].record()
+        H.hapi_extract(r.desc, r.packed, xd, batch, 18, out)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ts.append(ev[0].elapsed_time(ev[1]))
+    ext_ms = sorted(ts)[len(ts) // 2]
+    ratio = prof_ms / ext_ms
+    print(f"profile b{batch} chunk {chunk} inflight {inflight}: sum of layers {prof_ms:.3f} ms, "
+          f"extraction {ext_ms:.3f} ms, ratio {ratio:.2f}", flush=True)
+    lo, hi = (0.9, 2.5) if batch >= 128 and chunk == 0 and inflight == 0 else (0.8, 1.5)
+    assert lo <= ratio <= hi
 
 
 def test_kernel_stats_count_launches():

@@ -134,12 +134,30 @@ def test_workspace_holds_one_slot_set_per_partition_in_flight():
     for k in (2, 3, 4):
         assert H.hapi_workspace_bytes(d.set(inflight=k), 128, 18) == k * one
     assert H.hapi_workspace_bytes(d.set(inflight=4), 32, 18) == 2 * one  # only 2 partitions
-    # automatic: 2 x 128-image partitions need what 1 x 256 needs
+    # automatic: 2 x 128-image partitions need what 1 x 256 needs, plus the
+    # second partition's four guard gaps
     auto = _desc("resnet50")
     seq = _desc("resnet50", chunk=256)
-    assert H.hapi_workspace_bytes(auto, 256, 18) == H.hapi_workspace_bytes(seq, 256, 18)
+    assert H.hapi_workspace_bytes(auto, 256, 18) == H.hapi_workspace_bytes(seq, 256, 18) + 4 * H.HAPI_GUARD_BYTES
     _raises(H.HAPI_E_INVAL, H.hapi_workspace_bytes, d.set(inflight=5), 128, 18)
     _raises(H.HAPI_E_INVAL, H.hapi_workspace_bytes, d.set(inflight=-1), 128, 18)
+
+
+@pytest.mark.parametrize("name,batch,chunk,inflight", [("resnet50", 256, 0, 0), ("resnet50", 40, 16, 0),
+                                                       ("resnet18", 64, 0, 3), ("vit_b16", 5, 0, 0)])
+def test_workspace_guard_gaps(name, batch, chunk, inflight):
+    """Four gaps per partition in flight, each after one of the lane's
+    regions: ordered, disjoint and inside the workspace."""
+    d = _desc(name, chunk=chunk, inflight=inflight)
+    n = d.n_layers
+    ws = H.hapi_workspace_bytes(d, batch, n)
+    g = H.hapi_workspace_guards(d, batch, n)
+    parts = H.hapi_chunk_count(d, batch)
+    lanes = min(inflight or (2 if chunk == 0 and batch >= 128 else 1), parts)
+    assert len(g) == 4 * lanes
+    assert all(b - a >= H.HAPI_GUARD_BYTES for a, b in zip(g, g[1:]))
+    assert g[-1] + H.HAPI_GUARD_BYTES == ws
+    assert H.hapi_workspace_guards(d, batch, 0) == []
 
 
 def _raises(code, fn, *a):
