@@ -158,6 +158,8 @@ def main():
     ap.add_argument("--chunk", type=int, default=0)
     ap.add_argument("--inflight", type=int, default=0,
                     help="partitions in flight on separate streams (0: the library chooses)")
+    ap.add_argument("--direct", action="store_true",
+                    help="launch every kernel on every step (no replay of a captured HIP graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="time the library's plain copy (split 0) instead, for counter calibration")
@@ -188,7 +190,8 @@ def main():
     layers = PM.FACTORIES[cfg["model"]]()
     B = cfg["batch"]
     stream = torch.cuda.current_stream()
-    desc = H.Desc(layers, cfg["dtype"], stream=stream, chunk=args.chunk, inflight=args.inflight)
+    desc = H.Desc(layers, cfg["dtype"], stream=stream, chunk=args.chunk, inflight=args.inflight,
+                  direct=int(args.direct))
     tdt = torch.bfloat16 if cfg["dtype"] == H.HAPI_BF16 else torch.float32
 
     raw = torch.from_numpy(synth.flatten(synth.params(cfg["seed"], PM.raw_manifest(layers)))).cuda()
@@ -267,7 +270,8 @@ def main():
                    "batch": B, "split_layer": split, "image": "3x224x224",
                    "chunk": args.chunk or "auto",
                    "partitions": H.hapi_chunk_count(desc, B),
-                   "inflight": args.inflight or "auto"},
+                   "inflight": args.inflight or "auto",
+                   "launch": "direct" if args.direct else "graph replay"},
         "mfma_util_pct": mfma_util,
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                      "frac": round(achieved / peak, 4),

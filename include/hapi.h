@@ -132,6 +132,9 @@ typedef struct {
   int32_t inflight;                   /* partitions in flight at once, 0..4; 0 = the
                                          library chooses: 2 when chunk == 0 and the
                                          batch has >= 128 images, else 1 (sequential) */
+  int32_t direct;                     /* 0: repeated identical extractions replay a
+                                         captured HIP graph (see hapi_extract);
+                                         1: every call launches its kernels one by one */
 } hapi_model_desc;
 
 /* Raw (unpacked) weights: ONE flat float32 device buffer holding, layer by
@@ -223,7 +226,23 @@ int32_t hapi_chunk_count(const hapi_model_desc *desc, int32_t batch);
  * The batch runs as hapi_chunk_count() sequential partitions through the
  * workspace.  Errors: HAPI_E_INVAL (null pointer, batch < 1, split out of
  * range), HAPI_E_NOMEM (workspace too small), HAPI_E_UNSUPPORTED,
- * HAPI_E_DEVICE (a launch failed).  Asynchronous on desc->stream. */
+ * HAPI_E_DEVICE (a launch failed).  Asynchronous on desc->stream.
+ *
+ * Plan replay (desc->direct == 0).  A call identical to the previous
+ * extraction on the same host thread (same layers, dtype, input shape, chunk,
+ * inflight, device, pointers, batch and layer range) is captured once as a
+ * HIP graph -- every kernel launch of the call with its fork and join of the
+ * auxiliary streams -- and the graph is launched on desc->stream; later
+ * identical calls launch that graph again (the library keeps the 8 most
+ * recent graphs per host thread until the process ends).  The graph runs the
+ * same kernels with the same arguments, so results are bit-identical to
+ * direct launches; it only removes the per-kernel launch cost (which bounds
+ * small batches; Storage-side batch size adaptation asks throughput to hold
+ * at every batch).  A graph reads the pointers it was captured with: contents
+ * may change between calls, buffers must not be freed while a call that
+ * uses them is pending (as with direct launches).  Calls made while kernel
+ * statistics are enabled always launch directly.  The graph has no memset
+ * nodes. */
 int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *images,
                  int32_t batch, int32_t split_layer, void *out);
 

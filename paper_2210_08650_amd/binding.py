@@ -55,7 +55,8 @@ class hapi_model_desc(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32),
                 ("in_w", ctypes.c_int32), ("stream", ctypes.c_void_p),
                 ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
-                ("chunk", ctypes.c_int32), ("inflight", ctypes.c_int32)]
+                ("chunk", ctypes.c_int32), ("inflight", ctypes.c_int32),
+                ("direct", ctypes.c_int32)]
 
 
 class hapi_kernel_stat(ctypes.Structure):
@@ -177,7 +178,7 @@ class Desc:
     """Owns a ``hapi_model_desc`` and the layer array it points to."""
 
     def __init__(self, layers, dtype, in_shape=(3, 224, 224), stream=None, workspace=None,
-                 workspace_bytes=0, chunk=0, inflight=0):
+                 workspace_bytes=0, chunk=0, inflight=0, direct=0):
         self._layers = (hapi_layer * len(layers))()
         for i, spec in enumerate(layers):
             if isinstance(spec, hapi_layer):
@@ -191,9 +192,10 @@ class Desc:
         self.c.dtype = dtype
         self.c.in_c, self.c.in_h, self.c.in_w = in_shape
         self.set(stream=stream, workspace=workspace, workspace_bytes=workspace_bytes, chunk=chunk,
-                 inflight=inflight)
+                 inflight=inflight, direct=direct)
 
-    def set(self, stream=None, workspace=None, workspace_bytes=None, chunk=None, inflight=None):
+    def set(self, stream=None, workspace=None, workspace_bytes=None, chunk=None, inflight=None,
+            direct=None):
         if stream is not None:
             self.c.stream = _stream(stream)
         if workspace is not None:
@@ -208,6 +210,8 @@ class Desc:
             self.c.chunk = int(chunk)
         if inflight is not None:
             self.c.inflight = int(inflight)
+        if direct is not None:
+            self.c.direct = int(direct)
         return self
 
     @property

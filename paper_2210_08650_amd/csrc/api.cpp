@@ -110,6 +110,7 @@ int analyze(const hapi_model_desc *d, Model &m) {
   if (d->chunk < 0) return fail(HAPI_E_INVAL, "chunk must be >= 0");
   if (d->inflight < 0 || d->inflight > kMaxInflight)
     return fail(HAPI_E_INVAL, "inflight must be in [0, %d]", kMaxInflight);
+  if (d->direct != 0 && d->direct != 1) return fail(HAPI_E_INVAL, "direct must be 0 or 1");
   m = Model();
   m.bf16 = d->dtype == HAPI_BF16;
   m.esz = m.bf16 ? 2 : 4;
@@ -1034,6 +1035,111 @@ int run_batch(const hapi_model_desc *d, const Model &m, const void *weights, con
   return r;
 }
 
+// ------------------------------------------------------------- plan replay
+
+// Everything that determines the kernel launches of an extraction.
+struct PlanKey {
+  std::vector<hapi_layer> layers;
+  int32_t dtype = 0, in_c = 0, in_h = 0, in_w = 0, chunk = 0, inflight = 0;
+  const void *weights = nullptr, *images = nullptr, *out = nullptr, *ws = nullptr;
+  int batch = 0, start = 0, split = 0, dev = -1;
+
+  bool operator==(const PlanKey &o) const {
+    return dtype == o.dtype && in_c == o.in_c && in_h == o.in_h && in_w == o.in_w && chunk == o.chunk &&
+           inflight == o.inflight && weights == o.weights && images == o.images && out == o.out &&
+           ws == o.ws && batch == o.batch && start == o.start && split == o.split && dev == o.dev &&
+           layers.size() == o.layers.size() &&
+           std::memcmp(layers.data(), o.layers.data(), layers.size() * sizeof(hapi_layer)) == 0;
+  }
+};
+
+struct Plan {
+  PlanKey key;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
+// Per host thread: the key of the previous extraction, the captured plans
+// (most recent first) and a private stream per device to capture on (the
+// caller's stream may be the null stream, which cannot be captured).  Never
+// freed: graphs stay valid until the process ends, and destroying them from a
+// thread-exit destructor could run after the HIP runtime has shut down.
+struct PlanCache {
+  PlanKey last;
+  bool has_last = false;
+  std::vector<Plan> plans;
+  std::vector<hipStream_t> capture;  // per device
+};
+constexpr size_t kMaxPlans = 8;
+
+PlanCache &plan_cache() {
+  static thread_local PlanCache *pc = new PlanCache();
+  return *pc;
+}
+
+// Runs the extraction through the plan cache: replays a captured graph, or
+// captures one when the same call was made just before, or launches directly.
+int run_planned(const hapi_model_desc *desc, const Model &m, const void *weights, const void *images,
+                int batch, int start, int split, void *out, uint8_t *ws, int chunk, int lanes) {
+  hipStream_t s = static_cast<hipStream_t>(desc->stream);
+  PlanKey k;
+  k.layers.assign(desc->layers, desc->layers + desc->n_layers);
+  k.dtype = desc->dtype; k.in_c = desc->in_c; k.in_h = desc->in_h; k.in_w = desc->in_w;
+  k.chunk = desc->chunk; k.inflight = desc->inflight;
+  k.weights = weights; k.images = images; k.out = out; k.ws = ws;
+  k.batch = batch; k.start = start; k.split = split;
+  HIP_TRY(hipStreamGetDevice(s, &k.dev));
+  PlanCache &pc = plan_cache();
+  for (size_t i = 0; i < pc.plans.size(); ++i) {
+    if (!(pc.plans[i].key == k)) continue;
+    std::rotate(pc.plans.begin(), pc.plans.begin() + i, pc.plans.begin() + i + 1);
+    pc.has_last = false;
+    HIP_TRY(hipGraphLaunch(pc.plans[0].exec, s));
+    return HAPI_OK;
+  }
+  if (!pc.has_last || !(pc.last == k)) {
+    pc.last = std::move(k);
+    pc.has_last = true;
+    return run_batch(desc, m, weights, images, batch, start, split, out, ws, chunk, lanes, lanes, nullptr);
+  }
+  // Second identical call in a row: capture it on this thread's private
+  // stream of the device, then launch the graph on the caller's stream.
+  pc.has_last = false;
+  const int dev = k.dev;
+  if ((int)pc.capture.size() <= dev) pc.capture.resize(dev + 1, nullptr);
+  if (!pc.capture[dev]) HIP_TRY(hipStreamCreateWithFlags(&pc.capture[dev], hipStreamNonBlocking));
+  hapi_model_desc dc = *desc;
+  dc.stream = pc.capture[dev];
+  HIP_TRY(hipStreamBeginCapture(pc.capture[dev], hipStreamCaptureModeThreadLocal));
+  const int r = run_batch(&dc, m, weights, images, batch, start, split, out, ws, chunk, lanes, lanes, nullptr);
+  Plan p;
+  p.key = std::move(k);
+  const hipError_t e = hipStreamEndCapture(pc.capture[dev], &p.graph);
+  if (r != HAPI_OK) {
+    if (p.graph) (void)hipGraphDestroy(p.graph);
+    return r;
+  }
+  if (e != hipSuccess) return fail(HAPI_E_DEVICE, "hipStreamEndCapture failed: %s", hipGetErrorString(e));
+  const hipError_t ie = hipGraphInstantiate(&p.exec, p.graph, nullptr, nullptr, 0);
+  if (ie != hipSuccess) {
+    (void)hipGraphDestroy(p.graph);
+    return fail(HAPI_E_DEVICE, "hipGraphInstantiate failed: %s", hipGetErrorString(ie));
+  }
+  if (pc.plans.size() == kMaxPlans) {
+    (void)hipGraphExecDestroy(pc.plans.back().exec);
+    (void)hipGraphDestroy(pc.plans.back().graph);
+    pc.plans.pop_back();
+  }
+  pc.plans.insert(pc.plans.begin(), std::move(p));
+  HIP_TRY(hipGraphLaunch(pc.plans[0].exec, s));
+  return HAPI_OK;
+}
+
+bool stats_enabled() {
+  std::lock_guard<std::mutex> g(g_stats_mu);
+  return g_stats_on;
+}
+
 }  // namespace
 }  // namespace hapi
 
@@ -1184,6 +1290,9 @@ int extract_range(const hapi_model_desc *desc, const void *weights, const void *
     return fail(HAPI_E_NOMEM, "workspace of %zu bytes, %lld needed", desc->workspace_bytes,
                 (long long)need);
   if ((uintptr_t)desc->workspace % kAlign) return fail(HAPI_E_INVAL, "workspace must be 256-byte aligned");
+  if (desc->direct == 0 && !stats_enabled())
+    return run_planned(desc, m, weights, images, batch, start_layer, split_layer, out,
+                       static_cast<uint8_t *>(desc->workspace), chunk, lanes);
   return run_batch(desc, m, weights, images, batch, start_layer, split_layer, out,
                    static_cast<uint8_t *>(desc->workspace), chunk, lanes, lanes, nullptr);
 }

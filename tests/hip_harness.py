@@ -69,7 +69,9 @@ class Runner:
     def __init__(self, layers, dtype, params, in_shape=(3, 224, 224)):
         self.layers, self.dtype, self.in_shape = layers, dtype, tuple(in_shape)
         self.stream = torch.cuda.current_stream()
-        self.desc = H.Desc(layers, dtype, in_shape, stream=self.stream)
+        # direct launches: each call here uses fresh buffers, so none would
+        # replay a captured graph anyway (plan replay has a test of its own)
+        self.desc = H.Desc(layers, dtype, in_shape, stream=self.stream, direct=1)
         raw = torch.from_numpy(synth.flatten(params)).cuda()
         assert raw.numel() == H.hapi_raw_weight_count(self.desc)
         # zeroed, so that the alignment gaps the packer skips compare equal

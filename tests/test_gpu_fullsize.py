@@ -59,7 +59,7 @@ def test_resnet50_batch_512_two_full_partitions():
     r = Runner(PM.resnet50(), H.HAPI_BF16, ps)
     assert H.hapi_chunk_count(r.desc.set(chunk=0, inflight=0), 512) == 2
     got = r.extract_np(xd, 18)
-    idx = [0, 300, 511]
+    idx = samples(512)
     ref = om.forward(ps, xv[idx], 18)
     for j, i in enumerate(idx):
         err = rel_l2(got[i], ref[j])

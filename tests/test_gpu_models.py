@@ -14,7 +14,7 @@ import paper_2210_08650_amd as H
 from paper_2210_08650_amd import models as PM
 import synth
 from oracle import models as OM
-from tests.hip_harness import Runner, images_for, rel_l2
+from tests.hip_harness import Guarded, Runner, images_for, rel_l2
 
 pytestmark = pytest.mark.gpu
 
@@ -399,3 +399,42 @@ def test_window_average_pooling_is_exact(c, hw):
     got = r.extract(xd, 1).float().cpu().numpy()
     om = OM.Model("pool", [OM.AvgPool(2, 2)], shape)
     assert np.array_equal(got, om.forward([], xv, 1).astype(np.float32))
+
+
+@pytest.mark.parametrize("name,batch,split,chunk", [("resnet50", 8, 18, 0), ("resnet50", 128, 18, 0),
+                                                    ("vit_b16", 6, 10, 2), ("densenet121", 4, 12, 0)])
+def test_plan_replay_is_bit_exact(name, batch, split, chunk):
+    """Repeated identical extractions replay a captured HIP graph: every
+    replay must equal the direct launches bit for bit, with the program's own
+    GPU work and synchronisations between the replays, and must read the
+    current contents of its buffers (new images between replays give the
+    direct result for those images)."""
+    r, _, _, xd, _, _ = _setup(name, 74, batch)
+    direct = r.extract(xd, split, chunk=chunk)          # Runner launches directly each call
+    other = torch.flip(xd, dims=[0]).contiguous()
+    direct_other = r.extract(other, split, chunk=chunk)
+    d = H.Desc(r.layers, r.dtype, r.in_shape, stream=torch.cuda.current_stream(), chunk=chunk)
+    need = H.hapi_workspace_bytes(d, batch, split)
+    ws = Guarded(need, H.hapi_workspace_guards(d, batch, split))
+    d.set(workspace=ws.body, workspace_bytes=need)
+    img = xd.clone()
+    gout = Guarded(direct.numel() * direct.element_size())
+    out = gout.view(direct.dtype, tuple(direct.shape))
+    a = torch.randn(512, 512, device="cuda")
+    for it in range(6):   # 1st: direct, 2nd: captured and launched, then replays
+        out.fill_(0)
+        use_other = it == 4
+        img.copy_(other if use_other else xd)
+        H.hapi_extract(d, r.packed, img, batch, split, out)
+        b = a @ a                       # eager work of the program between replays
+        torch.cuda.synchronize()
+        assert torch.isfinite(b).all()
+        assert torch.equal(out, direct_other if use_other else direct), it
+    ws.check()
+    gout.check()
+    # direct = 1 never captures; the result is the same
+    d.set(direct=1)
+    out.fill_(0)
+    H.hapi_extract(d, r.packed, img, batch, split, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out, direct)
