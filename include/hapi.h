@@ -246,6 +246,30 @@ int32_t hapi_chunk_count(const hapi_model_desc *desc, int32_t batch);
 int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *images,
                  int32_t batch, int32_t split_layer, void *out);
 
+/* hapi_extract for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments and results as hapi_extract (bit-identical outputs), but
+ * desc->workspace and desc->workspace_bytes are ignored and the library's own
+ * device scratch is used instead -- a static array of
+ * HAPI_NOALLOC_SCRATCH_BYTES per GPU, part of the library's code object,
+ * held by each GPU the library runs on until the process ends.  The call
+ * allocates nothing (no hipMalloc/hipFree, no stream, event or graph
+ * creation): its partitions run one after another on desc->stream, with
+ * direct kernel launches.  The first call on a device, with that device
+ * current, looks up the scratch's address on it.
+ *   Errors: as hapi_extract; HAPI_E_NOMEM when the extraction needs more
+ *   than HAPI_NOALLOC_SCRATCH_BYTES of workspace (hapi_workspace_bytes with
+ *   desc->inflight = 1 tells how much; lower the batch or desc->chunk);
+ *   HAPI_E_INVAL when desc->stream is not on the current device.
+ *   Every call on one GPU shares that GPU's scratch: calls that overlap on a
+ *   GPU (different streams or host threads) race and give wrong results;
+ *   order them.  Nothing in the scratch needs to start at zero (every region
+ *   is written before it is read), so the contents a previous call left do
+ *   not matter. */
+#define HAPI_NOALLOC_SCRATCH_BYTES ((int64_t)256 << 20)
+int hapi_extract_noalloc(const hapi_model_desc *desc, const void *weights, const void *images,
+                         int32_t batch, int32_t split_layer, void *out);
+
 /* Resume from a split (the compute-tier half: System implementation, models
  * that run the forward pass between arbitrary layers; Design, "Request flow",
  * the client continues from the split layer's output).  Runs layers

@@ -29,7 +29,8 @@ __all__ = ["HapiError", "Desc", "hapi_layer", "hapi_model_desc", "hapi_kernel_st
            "HAPI_BATCHNORM", "LIB_PATH", "EXPORTED",
            "hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
            "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-           "hapi_workspace_guards", "HAPI_GUARD_BYTES", "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
+           "hapi_workspace_guards", "HAPI_GUARD_BYTES", "hapi_extract_range",
+           "hapi_extract_noalloc", "HAPI_NOALLOC_SCRATCH_BYTES", "hapi_profile_layers", "hapi_profile_memory",
            "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error", "hapi_split_job", "hapi_split_estimate", "hapi_split_choice", "hapi_choose_split"]
 
 _STATUS = {HAPI_E_INVAL: "HAPI_E_INVAL", HAPI_E_UNSUPPORTED: "HAPI_E_UNSUPPORTED",
@@ -129,6 +130,7 @@ def _load():
         "hapi_workspace_guards": (i32, [D, i32, i32, ctypes.POINTER(i64), i32]),
         "hapi_extract": (ctypes.c_int, [D, vp, vp, i32, i32, vp]),
         "hapi_extract_range": (ctypes.c_int, [D, vp, vp, i32, i32, i32, vp]),
+        "hapi_extract_noalloc": (ctypes.c_int, [D, vp, vp, i32, i32, vp]),
         "hapi_profile_layers": (ctypes.c_int, [D, i32, ctypes.POINTER(i64),
                                                ctypes.POINTER(ctypes.c_float)]),
         "hapi_profile_memory": (ctypes.c_int, [D, i32, ctypes.POINTER(i64)]),
@@ -148,7 +150,7 @@ def _load():
 _lib = _load()
 EXPORTED = ("hapi_raw_weight_count", "hapi_packed_weight_bytes", "hapi_pack_weights",
             "hapi_layer_shape", "hapi_workspace_bytes", "hapi_chunk_count", "hapi_extract",
-            "hapi_workspace_guards", "hapi_extract_range", "hapi_profile_layers", "hapi_profile_memory",
+            "hapi_workspace_guards", "hapi_extract_range", "hapi_extract_noalloc", "hapi_profile_layers", "hapi_profile_memory",
             "hapi_stats_enable", "hapi_stats_collect", "hapi_last_error", "hapi_choose_split")
 
 
@@ -265,6 +267,14 @@ def hapi_chunk_count(desc: Desc, batch: int) -> int:
 def hapi_extract(desc: Desc, weights, images, batch: int, split_layer: int, out) -> None:
     _check(_lib.hapi_extract(desc.ref, _ptr(weights), _ptr(images), int(batch),
                              int(split_layer), _ptr(out)))
+
+
+HAPI_NOALLOC_SCRATCH_BYTES = 256 << 20
+
+
+def hapi_extract_noalloc(desc: Desc, weights, images, batch: int, split_layer: int, out) -> None:
+    _check(_lib.hapi_extract_noalloc(desc.ref, _ptr(weights), _ptr(images), int(batch),
+                                     int(split_layer), _ptr(out)))
 
 
 def hapi_extract_range(desc: Desc, weights, input, batch: int, start_layer: int,

@@ -1260,8 +1260,40 @@ int hapi_pack_weights(const hapi_model_desc *desc, const void *raw_weights, void
 
 namespace {
 
+// Device scratch of hapi_extract_noalloc: one copy per GPU the library runs
+// on, held until the process ends.  In host code `scratch` only names the
+// symbol; its device address comes from hipGetSymbolAddress, per device.
+constexpr int64_t kScratchBytes = HAPI_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// The address of `scratch` on the current device `dev`, looked up once per
+// device (with that device current) and kept; null on failure.
+uint8_t *scratch_on(int dev) {
+  static std::mutex mu;
+  static uint8_t *ptr[64] = {};
+  if (dev < 0 || dev >= 64) {
+    fail(HAPI_E_DEVICE, "device %d outside the %d the static scratch supports", dev, 64);
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> g(mu);
+  if (!ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      fail(HAPI_E_DEVICE, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+      return nullptr;
+    }
+    ptr[dev] = static_cast<uint8_t *>(p);
+  }
+  return ptr[dev];
+}
+
+// use_scratch: the workspace is the library's static scratch (desc->workspace
+// and desc->workspace_bytes are ignored); partitions run one at a time on
+// desc->stream with direct launches, so the call creates no HIP object.
 int extract_range(const hapi_model_desc *desc, const void *weights, const void *images,
-                  int32_t batch, int32_t start_layer, int32_t split_layer, void *out) {
+                  int32_t batch, int32_t start_layer, int32_t split_layer, void *out,
+                  bool use_scratch = false) {
   Model m;
   int r = analyze(desc, m);
   if (r != HAPI_OK) return r;
@@ -1284,6 +1316,19 @@ int extract_range(const hapi_model_desc *desc, const void *weights, const void *
   const int chunk = chunk_for(desc, m, batch);
   if ((int64_t)chunk * max_tmp(m, split_layer) >= kIndexLimit)
     return fail(HAPI_E_UNSUPPORTED, "a partition of %d images exceeds 2^31 elements; lower chunk", chunk);
+  if (use_scratch) {
+    const int64_t need = workspace_for(m, split_layer, chunk, false, batch, 1);
+    if (need > kScratchBytes)
+      return fail(HAPI_E_NOMEM, "%lld workspace bytes needed, the static scratch holds %lld; "
+                  "use hapi_extract with a caller workspace", (long long)need, (long long)kScratchBytes);
+    int dev = -1, cur = -1;
+    HIP_TRY(hipStreamGetDevice(s, &dev));
+    HIP_TRY(hipGetDevice(&cur));
+    if (dev != cur) return fail(HAPI_E_INVAL, "desc->stream belongs to device %d, current device is %d", dev, cur);
+    uint8_t *ws = scratch_on(dev);
+    if (!ws) return HAPI_E_DEVICE;
+    return run_batch(desc, m, weights, images, batch, start_layer, split_layer, out, ws, chunk, 1, 1, nullptr);
+  }
   const int lanes = lanes_for(desc, chunk, batch);
   const int64_t need = workspace_for(m, split_layer, chunk, false, batch, lanes);
   if (!desc->workspace || (int64_t)desc->workspace_bytes < need)
@@ -1309,6 +1354,11 @@ int hapi_extract(const hapi_model_desc *desc, const void *weights, const void *i
 int hapi_extract_range(const hapi_model_desc *desc, const void *weights, const void *input,
                        int32_t batch, int32_t start_layer, int32_t end_layer, void *out) {
   return extract_range(desc, weights, input, batch, start_layer, end_layer, out);
+}
+
+int hapi_extract_noalloc(const hapi_model_desc *desc, const void *weights, const void *images,
+                         int32_t batch, int32_t split_layer, void *out) {
+  return extract_range(desc, weights, images, batch, 0, split_layer, out, true);
 }
 
 int hapi_profile_memory(const hapi_model_desc *desc, int32_t batch, int64_t *bytes) {
