@@ -534,10 +534,15 @@ struct PreAct {
   int lda = 0;
 };
 
+// out_hw > 0: y is the split output in the caller's NCHW layout (see
+// ConvArgs::out_hw); the launch returns hipErrorNotSupported, having launched
+// nothing, when the layer's kernel cannot store it.
 hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &in, int nb,
                     void *y, const void *res, bool relu, bool gelu, bool nchw_input, int ldc = 0,
-                    const void *x2 = nullptr, const Act *in2 = nullptr, PreAct pre = PreAct{}) {
+                    const void *x2 = nullptr, const Act *in2 = nullptr, PreAct pre = PreAct{},
+                    int out_hw = 0) {
   ConvArgs a{};
+  a.out_hw = out_hw;
   a.cus = c.cus;
   // Every other convolution of a partition walks its tiles backwards, so it
   // starts on the rows its producer wrote last, the ones most likely still in
@@ -607,6 +612,7 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
                                           (double)a.N * a.K + (cs.fused ? (double)a.M * cs.cin2 : 0.0));
   if (c.m.bf16)
     return timed(c.s, F_CONV_BF16, flops, bytes, [&] { return launch_conv_bf16(a, ld, c.s); });
+  if (out_hw) return hipErrorNotSupported;
   a.splits = cs.splits;
   a.part = c.part;
   hipError_t r = timed(c.s, F_CONV_F32, flops, bytes, [&] { return launch_conv_f32(a, ld, c.s); });
@@ -679,6 +685,28 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
     cur = c.slot[0];
     cur_slot = 0;
   }
+  // The split layer's last convolution stores the split output in the
+  // caller's NCHW layout itself when its kernel can (no separate layout pass);
+  // `stored` records that it did.
+  const Act &split_act = m.layers[split - 1].out;
+  void *const nchw_out = (out && bf && !layout_free(split_act)) ? out : nullptr;
+  bool stored = false;
+  // Runs the last convolution of layer li: into `out` as NCHW when li is the
+  // split layer and the kernel supports it, else into slot `dst` with `res`.
+  auto last_conv = [&](int li, const ConvSpec &cs, const void *x, const Act &in, int dst, const void *res,
+                       bool relu, const void *x2 = nullptr, const Act *in2 = nullptr) -> int {
+    if (nchw_out && li == split - 1) {
+      const hipError_t e = run_conv(c, cs, x, in, nb, nchw_out, res, relu, false, false, 0, x2, in2, PreAct{},
+                                    split_act.h * split_act.w);
+      if (e == hipSuccess) {
+        stored = true;
+        return HAPI_OK;
+      }
+      if (e != hipErrorNotSupported) HIP_TRY(e);
+    }
+    HIP_TRY(run_conv(c, cs, x, in, nb, c.slot[dst], res, relu, false, false, 0, x2, in2));
+    return HAPI_OK;
+  };
   int li0 = start;
   // Stem convolution and max pooling in one kernel when the stem output is
   // not itself the split and layers are not being timed one by one.
@@ -725,8 +753,12 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
           src = c.slot[o];
           o = free_slot(o);
         }
-        HIP_TRY(run_conv(c, cs, src, lp.in, nb, c.slot[o], nullptr,
-                         L.kind == HAPI_CONV && L.relu, false, nchw_in));
+        if (!nchw_in && !cs.s2d && !cs.nhwc8) {
+          if (int r = last_conv(li, cs, src, lp.in, o, nullptr, L.kind == HAPI_CONV && L.relu)) return r;
+        } else {
+          HIP_TRY(run_conv(c, cs, src, lp.in, nb, c.slot[o], nullptr, L.kind == HAPI_CONV && L.relu, false,
+                           nchw_in));
+        }
         cur = c.slot[o];
         cur_slot = o;
         break;
@@ -759,8 +791,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
         if (lp.convs[1].fused) {  // conv2 and the projection shortcut in one GEMM
           const int B = free_slot(A);
-          HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], mid, nb, c.slot[B], nullptr, true, false, false, 0,
-                           cur, &lp.in));
+          if (int r = last_conv(li, lp.convs[1], c.slot[A], mid, B, nullptr, true, cur, &lp.in)) return r;
           cur = c.slot[B];
           cur_slot = B;
           break;
@@ -773,7 +804,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         }
         // In place over the block input: each output element's residual is read
         // by the same thread right before that element is written.
-        HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], mid, nb, c.slot[cur_slot], res, true, false, false));
+        if (int r = last_conv(li, lp.convs[1], c.slot[A], mid, cur_slot, res, true)) return r;
         cur = c.slot[cur_slot];
         break;
       }
@@ -802,8 +833,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         }
         HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], a1, nb, c.slot[B], nullptr, true, false, false));
         if (lp.convs[2].fused) {  // c3 and the projection shortcut in one GEMM, into the free slot
-          HIP_TRY(run_conv(c, lp.convs[2], c.slot[B], a2, nb, c.slot[A], nullptr, true, false, false, 0,
-                           cur, &lp.in));
+          if (int r = last_conv(li, lp.convs[2], c.slot[B], a2, A, nullptr, true, cur, &lp.in)) return r;
           cur = c.slot[A];
           cur_slot = A;
           break;
@@ -813,7 +843,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
           HIP_TRY(run_conv(c, lp.convs[3], cur, lp.in, nb, c.slot[A], nullptr, false, false, false));
           res = c.slot[A];
         }
-        HIP_TRY(run_conv(c, lp.convs[2], c.slot[B], a2, nb, c.slot[cur_slot], res, true, false, false));
+        if (int r = last_conv(li, lp.convs[2], c.slot[B], a2, cur_slot, res, true)) return r;
         cur = c.slot[cur_slot];
         break;
       }
@@ -942,7 +972,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
     }
     if (c.on_layer) c.on_layer(li, false);
   }
-  if (out) {
+  if (out && !stored) {
     const Act &o = m.layers[split - 1].out;
     const int64_t bytes = (int64_t)nb * o.elems() * m.esz;
     if (layout_free(o)) {

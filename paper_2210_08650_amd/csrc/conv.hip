@@ -648,16 +648,16 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   __syncthreads();
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
-  if (n >= a.N) return;
+  if (n >= a.N && !a.out_hw) return;
   float bias[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) bias[e] = a.bias ? a.bias[n + e] : 0.0f;
+  for (int e = 0; e < 8; ++e) bias[e] = (a.bias && n < a.N) ? a.bias[n + e] : 0.0f;
   uint16_t *y = static_cast<uint16_t *>(a.y);
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
     const int rr = t / CPR + k * RPP;
     const int m = m0 + rr;
-    if (m >= a.M) break;
+    if (m >= a.M || n >= a.N) break;
     const float4 p = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8);
     const float4 q = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8 + 4);
     // bias, then the residual: the order of every epilogue in the library
@@ -679,7 +679,26 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
       const float hi = epilogue_act(v[2 * e + 1], a.relu, a.gelu);
       o[e] = f2bf2(lo, hi);
     }
-    *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+    if (a.out_hw) {
+      // the finished chunk back into the first half of its own staging
+      // slot (no other thread reads that slot)
+      *reinterpret_cast<uint4 *>(Cs + rr * SM::kCPitch + cc * 8) = make_uint4(o[0], o[1], o[2], o[3]);
+    } else {
+      *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+  if (a.out_hw) {
+    // NCHW store: consecutive threads take consecutive rows (pixels) of one
+    // channel, which are consecutive addresses within an image.
+    __syncthreads();
+    const uint16_t *Cb = reinterpret_cast<const uint16_t *>(Cs);
+    for (int idx = t; idx < BM * BN; idx += NT) {
+      const int c = idx / BM, rr = idx - c * BM;
+      const int m = m0 + rr, nn = n0 + c;
+      if (m >= a.M || nn >= a.N) continue;
+      const int img = m / a.out_hw, px = m - img * a.out_hw;
+      y[((int64_t)img * a.N + nn) * a.out_hw + px] = Cb[rr * (2 * SM::kCPitch) + (c / 8) * 16 + (c % 8)];
+    }
   }
 }
 
@@ -997,15 +1016,15 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   __syncthreads();
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
-  if (n >= a.N) return;
+  if (n >= a.N && !a.out_hw) return;
   float bias[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) bias[e] = a.bias ? a.bias[n + e] : 0.0f;
+  for (int e = 0; e < 8; ++e) bias[e] = (a.bias && n < a.N) ? a.bias[n + e] : 0.0f;
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
     const int rr = t / CPR + k * RPP;
     const int m = m0 + rr;
-    if (m >= a.M) break;
+    if (m >= a.M || n >= a.N) break;
     const float4 p = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8);
     const float4 q = *reinterpret_cast<const float4 *>(Cs + rr * SM::kCPitch + cc * 8 + 4);
     // bias, then the residual: the order of every epilogue in the library
@@ -1027,7 +1046,26 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
       const float hi = epilogue_act(v[2 * e + 1], a.relu, a.gelu);
       o[e] = f2bf2(lo, hi);
     }
-    *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+    if (a.out_hw) {
+      // the finished chunk back into the first half of its own staging
+      // slot (no other thread reads that slot)
+      *reinterpret_cast<uint4 *>(Cs + rr * SM::kCPitch + cc * 8) = make_uint4(o[0], o[1], o[2], o[3]);
+    } else {
+      *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+  if (a.out_hw) {
+    // NCHW store: consecutive threads take consecutive rows (pixels) of one
+    // channel, which are consecutive addresses within an image.
+    __syncthreads();
+    const uint16_t *Cb = reinterpret_cast<const uint16_t *>(Cs);
+    for (int idx = t; idx < BM * BN; idx += NT) {
+      const int c = idx / BM, rr = idx - c * BM;
+      const int m = m0 + rr, nn = n0 + c;
+      if (m >= a.M || nn >= a.N) continue;
+      const int img = m / a.out_hw, px = m - img * a.out_hw;
+      y[((int64_t)img * a.N + nn) * a.out_hw + px] = Cb[rr * (2 * SM::kCPitch) + (c / 8) * 16 + (c % 8)];
+    }
   }
 }
 
@@ -1413,7 +1451,8 @@ __global__ __launch_bounds__(WM * WN * 64, MINB) void conv_bf16_short_kernel(Con
   constexpr int KS = BK / 16;
   constexpr int kStage = (BM + BN) * BK;
   constexpr int kWC = TN * 32;
-  static_assert(TM >= 1 && TN >= 1 && NA >= 1 && NB >= 1 && KT >= 1 && KT <= 2, "tile");
+  static_assert(TM >= 1 && TN >= 1 && NA >= 1 && NB >= 1 && KT >= 1 && KT <= 8, "tile");
+  static_assert(KT * (BM + BN) * BK * 2 + BN * 4 <= 163840, "LDS");
   __shared__ __attribute__((aligned(16))) uint16_t smem[KT * kStage];
   __shared__ __attribute__((aligned(16))) float bias_s[BN];
 
@@ -1608,8 +1647,22 @@ hipError_t launch_ws_ld(const ConvArgs &a, hipStream_t s) {
 
 // Tile shape per layer.  Every shape uses the same k-tile and MFMA, so the
 // choice never changes a result bit.
+// A split output stored as NCHW from the epilogue: the warp-specialised
+// kernel with the LDS-staged epilogue, in the tile shape the layer would get
+// (tile shapes never change results).
+template <int LD>
+hipError_t launch_nchw_out(const ConvArgs &a, hipStream_t s) {
+  if (!ws_eligible(a, (Loader)LD) || LD == LD_S2D || a.N % 8) return hipErrorNotSupported;
+  if (a.lanes <= 1 && a.N >= 64 && 2 * (int64_t)((a.M + 127) / 128) * ((a.N + 127) / 128) < a.cus)
+    return launch_ws_ld<64, 64, 2, 2, 4, LD, 0, 2>(a, s);
+  if (a.N <= 64) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+  if (a.res && a.N >= 1024) return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
+  return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+}
+
 template <int LD>
 hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
+  if (a.out_hw > 0) return launch_nchw_out<LD>(a, s);
   // Measured on MI355X over the ResNet-50 conv shapes (per-layer kernel
   // traces of every configuration above):
   // - the warp-specialised kernel with two workgroups per CU (128 x 64 tiles)
@@ -1919,6 +1972,9 @@ hipError_t launch_f32_cfg(const ConvArgs &a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
+  if (a.out_hw > 0 && ((ld != LD_GEMM && ld != LD_NHWC && ld != LD_CAT) || a.pre_scale || (a.lda && a.lda != a.K) ||
+                       a.gelu || a.N % 8 || a.ldr % 8))
+    return hipErrorNotSupported;
   if (a.pre_scale || (a.lda && a.lda != a.K)) {
     // Pre-activated or strided A (a channel prefix of a wider tensor): the
     // pipelined kernel, whose loader zero-fills the ragged last k-tile.
@@ -1944,7 +2000,7 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
     // The pipelined kernel needs 16-byte output rows; the register-staged one
     // handles element gathers (NCHW stems) and any other width.
     case LD_NHWC:
-      if (!a.gelu && a.Ho == a.H && a.Wo == a.W && conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
+      if (!a.gelu && !a.out_hw && a.Ho == a.H && a.Wo == a.W && conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
         return launch_conv3x3_c64(a.x, a.w, a.Kp, a.bias, a.res, a.ldr, a.y, a.ldc, a.n_img, a.H, a.W, a.relu != 0,
                                   a.cus > 0 ? a.cus : cu_count(), s);
       return (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) ? launch_pipe_ld<LD_NHWC>(a, s)

@@ -100,6 +100,11 @@ struct ConvArgs {
   // Partitions in flight on the device (kernels of the others may fill the
   // CUs this launch leaves idle); tile choice only, never the results.
   int lanes;
+  // > 0: y is the caller's NCHW tensor [n][N][out_hw] (a split output stored
+  // from the epilogue, out_hw = Ho * Wo); 0: NHWC rows y[M][ldc].  bf16 only;
+  // launch_conv_bf16 returns hipErrorNotSupported when the layer's kernel
+  // cannot store it, before launching anything.
+  int out_hw;
   // fp32 only: the k-tiles split into `splits` consecutive slices computed by
   // separate workgroups into part [splits][M][N] (float32), then summed in
   // slice order (fixed, so results do not depend on M); splits <= 1: none.

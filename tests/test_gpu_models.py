@@ -438,3 +438,32 @@ def test_plan_replay_is_bit_exact(name, batch, split, chunk):
     H.hapi_extract(d, r.packed, img, batch, split, out)
     torch.cuda.synchronize()
     assert torch.equal(out, direct)
+
+
+@pytest.mark.parametrize("name,split,batch", [("resnet50", 18, 8), ("resnet50", 18, 130), ("resnet50", 10, 3),
+                                              ("resnet18", 8, 5), ("resnet18", 5, 3), ("vgg16", 17, 2),
+                                              ("resnet50", 4, 2)])
+def test_split_output_stored_from_epilogue_is_bit_exact(name, split, batch):
+    """The split layer's last convolution stores the split output in the
+    caller's NCHW layout from its epilogue; it must equal, bit for bit, the
+    same layer's NHWC output put in NCHW by the library's separate layout
+    pass (the same model with an identity max pooling appended, so that the
+    convolution's output is no longer the split)."""
+    om = OM.build(name)
+    ps = synth.params(20, om.manifest())
+    counts = om.param_counts()
+    layers = PM.FACTORIES[name]()[:split]
+    dtype = H.HAPI_BF16
+    fused = Runner(layers, dtype, ps[:sum(counts[:split])])
+    plain = Runner(layers + [PM.maxpool(1, 1)], dtype, ps[:sum(counts[:split])])
+    xd, _ = images_for(dtype, synth.images(21, batch))
+    a = fused.extract(xd, split)
+    b = plain.extract(xd, split + 1)
+    H.hapi_stats_enable(True)
+    fused.extract(xd, split)
+    st = {s["name"]: s for s in H.hapi_stats_collect()}
+    H.hapi_stats_enable(False)
+    print(f"{name} split {split} b{batch}: {tuple(a.shape)}, layout passes {st.get('layout', {}).get('launches', 0)}",
+          flush=True)
+    assert a.shape == b.shape
+    assert torch.equal(a, b)
