@@ -39,6 +39,64 @@ def _cores():
     return min(n, int(omp)) if omp and omp.isdigit() else n
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def _sclk_now():
+    """Highest current shader clock (MHz) over the GPUs' sysfs DPM tables
+    (the line marked '*'), or None when unreadable."""
+    import glob
+    import re
+    best = None
+    for path in glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"):
+        try:
+            for line in open(path):
+                if "*" in line:
+                    m = re.search(r"(\d+)\s*[Mm][Hh]z", line)
+                    if m:
+                        best = max(best or 0, int(m.group(1)))
+        except OSError:
+            pass
+    return best
+
+
+def sustained_sclk(step, seconds=1.5):
+    """Median shader clock sampled every 20 ms while the workload runs back to
+    back for about `seconds` (outside the timed region)."""
+    import threading
+    import torch
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            v = _sclk_now()
+            if v:
+                samples.append(v)
+            time.sleep(0.02)
+
+    torch.cuda.synchronize()
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            step()
+        torch.cuda.synchronize()
+    stop.set()
+    th.join()
+    if not samples:
+        return None, 0
+    samples.sort()
+    return samples[len(samples) // 2], len(samples)
+
+
 def measured_traffic(workload):
     """HBM bytes per convolution launch from the committed rocprofv3 counter
     summary, or None when a convolution source changed since it was taken."""
@@ -79,7 +137,7 @@ def cpu_baseline(cfg, budget_s=15.0):
     t0 = time.perf_counter()
     om.forward(ps, imgs[1:1 + n], cfg["split"])
     dt = time.perf_counter() - t0
-    return {"value": round(n / dt, 4), "unit": "images/s", "cores": threads, "kind": "oracle",
+    return {"value": round(n / dt, 4), "unit": "images/s", "cores": threads, "cpu": cpu_model(), "kind": "oracle",
             "sample": f"{n} images of the same workload (images 1..{n}), float64 oracle, "
                       f"{dt:.1f} s"}
 
@@ -161,6 +219,8 @@ def main():
     ap.add_argument("--direct", action="store_true",
                     help="launch every kernel on every step (no replay of a captured HIP graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sclk", action="store_true",
+                    help="skip the sustained run that samples the shader clock (for profiler runs)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="time the library's plain copy (split 0) instead, for counter calibration")
     ap.add_argument("--concurrency", type=int, default=0,
@@ -250,6 +310,8 @@ def main():
     mfma_util = None if args.calib_copy else round(
         100.0 * dom["flops"] / args.steps / (ms_per_step * 1e-3) / 1e12 / peak, 2)
 
+    sclk, sclk_n = (None, 0) if args.calib_copy or args.no_sclk else sustained_sclk(step)
+
     default = args.workload == "resnet50_bf16_b256" and not args.batch and not args.calib_copy
     result = {
         "metric": ("feature-extraction images/sec to split layer (ResNet-50 bf16 b=256); MFMA util %"
@@ -273,7 +335,14 @@ def main():
                    "inflight": args.inflight or "auto",
                    "launch": "direct" if args.direct else "graph replay"},
         "mfma_util_pct": mfma_util,
+        # the same share against the peak at the shader clock measured while
+        # the workload ran (datasheet peaks assume 2.4 GHz)
+        "sclk_mhz": sclk,
+        "sclk_samples": sclk_n,
+        "mfma_util_pct_at_sclk": (round(mfma_util * 2400.0 / sclk, 2) if mfma_util is not None and sclk
+                                  else None),
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                     "peak_at_sclk": (round(peak * sclk / 2400.0, 1) if bound == "mfma" and sclk else None),
                      "frac": round(achieved / peak, 4),
                      "traffic": None if args.calib_copy or args.batch else measured_traffic(args.workload),
                      "algorithmic_bytes_per_launch": round(dom["bytes"] / dom["launches"]),
