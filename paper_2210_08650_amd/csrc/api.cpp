@@ -634,6 +634,19 @@ bool stem_pool_fusable(const Model &m) {
   return stem_pool_supported(l0.in.c, l0.in.h, l0.in.w, cs.cout, l0.out.h, l0.out.w, l1.out.h, l1.out.w);
 }
 
+// Layer li (a convolution) and layer li + 1 (2 x 2 / 2 max pooling) that one
+// kernel runs: 3 x 3, stride 1, padding 1, 64 channels to 64, ReLU, bf16.
+bool pool_fusable(const Model &m, int li) {
+  if (!m.bf16 || li + 1 >= (int)m.layers.size()) return false;
+  const LayerPlan &lp = m.layers[li], &pl = m.layers[li + 1];
+  if (lp.L.kind != HAPI_CONV || !lp.L.relu || lp.convs.size() != 1) return false;
+  const ConvSpec &cs = lp.convs[0];
+  if (cs.s2d || cs.nhwc8 || cs.fused) return false;
+  if (pl.L.kind != HAPI_MAXPOOL || pl.L.k != 2 || pl.L.stride != 2 || pl.L.pad != 0) return false;
+  return conv3x3_c64_supported(cs.cin, cs.cout, cs.k, cs.k, cs.stride, cs.pad, lp.in.w, cs.Kp, cs.cout, cs.cout) &&
+         conv3x3_c64_pool_supported(lp.in.h, lp.in.w, cs.cout);
+}
+
 // The tensor in front of layer `start` + 1: the input (start = 0) or the
 // output of layer `start`.
 const Act &act_at(const Model &m, int start) {
@@ -730,6 +743,26 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
     const hapi_layer &L = lp.L;
     if (c.on_layer) c.on_layer(li, true);
     const bool nchw_in = (li == 0) && m.first_reads_nchw;
+    // A 3 x 3 convolution over 64 channels to 64 with ReLU followed by 2 x 2 / 2
+    // max pooling (VGG's conv1_2 + pool1), when its own output is not the
+    // split and layers are not being timed one by one: one kernel pools the
+    // rounded result before storing it, bit for bit the two layers' output.
+    if (L.kind == HAPI_CONV && !nchw_in && !c.on_layer && li + 1 < split && pool_fusable(m, li)) {
+      const ConvSpec &cs = lp.convs[0];
+      const LayerPlan &pl = m.layers[li + 1];
+      const int o = free_slot();
+      const double flops = 2.0 * nb * lp.out.h * lp.out.w * (double)cs.cout * cs.K;
+      const double bytes = (double)m.esz * ((double)nb * (lp.in.elems() + pl.out.elems()) + (double)cs.cout * cs.Kp);
+      HIP_TRY(timed(c.s, F_CONV_BF16, flops, bytes, [&] {
+        return launch_conv3x3_c64(cur, c.pk + cs.pk_w, cs.Kp, reinterpret_cast<const float *>(c.pk + cs.pk_b), nullptr,
+                                  cs.cout, c.slot[o], cs.cout, nb, lp.in.h, lp.in.w, true, c.cus, c.s, nullptr, 0,
+                                  nullptr, true);
+      }));
+      cur = c.slot[o];
+      cur_slot = o;
+      ++li;  // the pooling layer ran inside the convolution
+      continue;
+    }
     switch (L.kind) {
       case HAPI_CONV:
       case HAPI_PATCH_EMBED: {

@@ -80,8 +80,14 @@ constexpr int kW3Pitch = kC + 8;         // bf16 pitch of an expansion weight ro
 // EXPAND = true: the expansion weights take the LDS of four ring rows; the
 // ring holds the 6 rows a step reads, and the next step's rows replace the 4
 // oldest after a barrier, while the expansion runs.
-template <bool EXPAND>
+// POOL = true (with EXPAND = false): the ReLU'd, rounded 3 x 3 result goes
+// through 2 x 2 / 2 max pooling before it is stored, y being the pooled
+// output [n, H/2, W/2][ldc] (H % 4 == 0, W even).  Each wave then computes two
+// output rows x 16 columns (lane % 32 = 16 dr + dc), so that a pooling
+// window's four pixels are lanes l, l ^ 1, l ^ 16 and l ^ 17 of one wave.
+template <bool EXPAND, bool POOL = false>
 __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
+  static_assert(!(EXPAND && POOL), "pooling follows the plain 3 x 3 only");
   constexpr int kRing = EXPAND ? 6 : kRows;
   __shared__ __attribute__((aligned(16))) uint16_t wts[kC * kWPitch];
   __shared__ __attribute__((aligned(16))) uint16_t ring[kRing * kPix * kC];
@@ -183,9 +189,11 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
           pre[q][e] = load_row(ho + 5 + q, t + e * kThreads);
         }
     }
-    const int row = ho + (wave & (kStepRows - 1));  // this wave's output row
-    const int pi = wave / kStepRows;                 // and its 32-pixel half
-    const int px = 32 * pi + lrow;  // ring pixel px + 1, output column c0 + px
+    // This lane's output pixel: row `row`, ring pixel px + 1, output column
+    // c0 + px.  Plain: the wave's row (ho + wave % 4) and 32-pixel half;
+    // POOL: rows ho + 2 (wave % 2) + lrow / 16, columns 16 (wave / 2) + lrow % 16.
+    const int row = POOL ? ho + 2 * (wave & 1) + (lrow >> 4) : ho + (wave & (kStepRows - 1));
+    const int px = POOL ? 16 * (wave >> 1) + (lrow & 15) : 32 * (wave / kStepRows) + lrow;
     const int64_t m = img_px + (int64_t)row * a.W + c0 + px;
     const bool live = row < r1 && c0 + px < a.W;
     // EXPAND: the residual of this lane's outputs, loaded now so that its
@@ -208,7 +216,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[j][e] = 0.0f;
-    if (row < r1) {
+    if (POOL ? ho < r1 : row < r1) {  // POOL: the step's four rows are all inside the band
       // Fragments are read kAhead k-steps before their MFMAs (a ring of
       // kAhead + 1 register sets), so the LDS latency hides behind 2 kAhead
       // MFMAs of this wave plus those of the other wave on the SIMD.
@@ -257,7 +265,43 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
         v[2 * e + 1] += __uint_as_float(w4[e] & 0xffff0000u);
       }
     };
-    if constexpr (!EXPAND) {
+    if constexpr (POOL) {
+      // Max over the window (lanes l, l ^ 1, l ^ 16, l ^ 17) of the rounded,
+      // non-negative bf16 values, compared as unsigned integers, as the
+      // separate pooling layer computes it; the window's top-left lane stores.
+      auto pmax = [](uint32_t x, uint32_t y) -> uint32_t {
+        return max(x & 0xffffu, y & 0xffffu) | (max(x >> 16, y >> 16) << 16);
+      };
+      if (ho < r1) {
+        const bool store = (lrow & 0x11) == 0 && c0 + px < a.W;
+        const int64_t pm = ((int64_t)img * (a.H / 2) + (row >> 1)) * (a.W / 2) + ((c0 + px) >> 1);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const int n = 32 * j + 16 * q + 8 * lh;
+            float v[8];
+            finish8(acc[j], q, bias_s + n, v);
+            uint32_t o[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              o[e] = f2bf2(fmaxf(v[2 * e], 0.0f), fmaxf(v[2 * e + 1], 0.0f));
+              o[e] = pmax(o[e], (uint32_t)__shfl_xor((int)o[e], 1, 64));
+              o[e] = pmax(o[e], (uint32_t)__shfl_xor((int)o[e], 16, 64));
+            }
+            if (store) *reinterpret_cast<uint4 *>(y + pm * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+          }
+      }
+      if (more) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < kPer; ++e) {
+            const int it = t + e * kThreads;
+            if (it < kRowChunks) store_row(ho + 5 + q, it, pre[q][e]);
+          }
+      }
+    } else if constexpr (!EXPAND) {
       if (row < r1) {
 #pragma unroll
         for (int j = 0; j < 2; ++j)
@@ -358,13 +402,16 @@ bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, in
          ldc % 8 == 0 && ldr % 8 == 0;
 }
 
+bool conv3x3_c64_pool_supported(int H, int W, int ldc) { return H % 4 == 0 && W % 2 == 0 && ldc % 8 == 0; }
+
 bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr) {
   return N3 == kExpand && K3 == kC && Kp3 == kC && ldc % 8 == 0 && ldr % 8 == 0;
 }
 
 hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float *bias, const void *res, int ldr,
                               void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s,
-                              const void *w3, int ldw3, const float *bias3) {
+                              const void *w3, int ldw3, const float *bias3, bool pool) {
+  if (pool && (w3 || res || !relu || !conv3x3_c64_pool_supported(H, W, ldc))) return hipErrorInvalidValue;
   // Enough workgroups to fill the CUs: split images into strips of columns,
   // then into bands of rows.
   const int strips = (W + kPix - 3) / (kPix - 2);
@@ -382,6 +429,8 @@ hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
   if (w3)
     hapi_launch(conv3x3_c64_kernel<true>, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
+  else if (pool)
+    hapi_launch((conv3x3_c64_kernel<false, true>), dim3((unsigned)grid), dim3(kThreads), 0, s, a);
   else
     hapi_launch(conv3x3_c64_kernel<false>, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
   return hipGetLastError();

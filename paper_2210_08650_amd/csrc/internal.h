@@ -176,9 +176,14 @@ bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, in
 // expanded in the same kernel by a 1 x 1 convolution to 256 channels with
 // bias3, the residual res [.][ldr] and ReLU, into y [.][ldc] (a bottleneck's
 // last two convolutions); see conv3x3_c64_expand_supported.
+// pool: the ReLU'd result goes through 2 x 2 / 2 max pooling first, y being
+// the pooled output [n, H/2, W/2][ldc] (relu, no residual, no expansion;
+// see conv3x3_c64_pool_supported).
 hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float *bias, const void *res, int ldr,
                               void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s,
-                              const void *w3 = nullptr, int ldw3 = 0, const float *bias3 = nullptr);
+                              const void *w3 = nullptr, int ldw3 = 0, const float *bias3 = nullptr,
+                              bool pool = false);
+bool conv3x3_c64_pool_supported(int H, int W, int ldc);
 bool conv3x3_c64_expand_supported(int N3, int K3, int Kp3, int ldc, int ldr);
 // First layer over an 8-slot NHWC input (LD_NHWC8) with 64 outputs, no
 // residual: weights in registers, operands loaded straight from memory.

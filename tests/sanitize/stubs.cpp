@@ -39,9 +39,10 @@ hipError_t launch_space_to_depth(const void *, void *, int, int, int, int, int, 
 }
 bool conv3x3_c64_supported(int, int, int, int, int, int, int, int, int, int) { return false; }
 hipError_t launch_conv3x3_c64(const void *, const void *, int, const float *, const void *, int, void *, int, int,
-                              int, int, bool, int, hipStream_t, const void *, int, const float *) {
+                              int, int, bool, int, hipStream_t, const void *, int, const float *, bool) {
   return none();
 }
+bool conv3x3_c64_pool_supported(int, int, int) { return false; }
 bool conv3x3_c64_expand_supported(int, int, int, int, int) { return false; }
 bool conv_first_supported(const ConvArgs &) { return false; }
 hipError_t launch_conv_first(const ConvArgs &, hipStream_t) { return none(); }

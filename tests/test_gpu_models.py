@@ -467,3 +467,27 @@ def test_split_output_stored_from_epilogue_is_bit_exact(name, split, batch):
           flush=True)
     assert a.shape == b.shape
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("shape,batch", [((64, 224, 224), 2), ((64, 20, 26), 3), ((64, 8, 130), 2)])
+def test_conv_pool_fused_is_bit_exact(shape, batch):
+    """A 3x3 64->64 convolution with ReLU followed by 2x2/2 max pooling (VGG's
+    conv1_2 and pool1) runs as one kernel that pools the rounded result before
+    storing it; it must equal, bit for bit, the convolution and the pooling
+    layer run separately (an identity pooling in between keeps them apart)."""
+    c = shape[0]
+    w = synth.params(22, [((c, c, 3, 3), "he"), ((c,), "bias")])
+    fused = Runner([PM.maxpool(1, 1), PM.conv(c, c, 3, 1, 1, bias=True, relu=True), PM.maxpool(2, 2)],
+                   H.HAPI_BF16, w, shape)
+    apart = Runner([PM.maxpool(1, 1), PM.conv(c, c, 3, 1, 1, bias=True, relu=True), PM.maxpool(1, 1),
+                    PM.maxpool(2, 2)], H.HAPI_BF16, w, shape)
+    xd, _ = images_for(H.HAPI_BF16, synth.images(23, batch, *shape))
+    H.hapi_stats_enable(True)
+    a = fused.extract(xd, 3)
+    st = {s["name"]: s for s in H.hapi_stats_collect()}
+    H.hapi_stats_enable(False)
+    b = apart.extract(xd, 4)
+    print(f"conv+pool {shape} b{batch}: {tuple(a.shape)}, separate pooling passes {st.get('maxpool', {}).get('launches', 0)}",
+          flush=True)
+    assert "maxpool" not in st or st["maxpool"]["launches"] == 1  # only the leading identity pooling
+    assert torch.equal(a, b)
