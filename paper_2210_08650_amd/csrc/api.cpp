@@ -913,7 +913,14 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], tokD, 1, c.slot[cur_slot], cur, false, false, false));
         HIP_TRY(ln(lp.extras[2], lp.extras[3], cur, c.slot[A]));
         HIP_TRY(run_conv(c, lp.convs[2], c.slot[A], tokD, 1, c.slot[B], nullptr, false, true, false));
-        HIP_TRY(run_conv(c, lp.convs[3], c.slot[B], tokF, 1, c.slot[cur_slot], cur, false, false, false));
+        // The split block's last linear layer writes the caller's [B, T, D]
+        // output itself (the token layout is the caller's layout).
+        if (out && li == split - 1) {
+          HIP_TRY(run_conv(c, lp.convs[3], c.slot[B], tokF, 1, out, cur, false, false, false));
+          stored = true;
+        } else {
+          HIP_TRY(run_conv(c, lp.convs[3], c.slot[B], tokF, 1, c.slot[cur_slot], cur, false, false, false));
+        }
         break;
       }
       case HAPI_LAYERNORM: {
