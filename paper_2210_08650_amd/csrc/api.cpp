@@ -540,9 +540,10 @@ struct PreAct {
 hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &in, int nb,
                     void *y, const void *res, bool relu, bool gelu, bool nchw_input, int ldc = 0,
                     const void *x2 = nullptr, const Act *in2 = nullptr, PreAct pre = PreAct{},
-                    int out_hw = 0) {
+                    int out_hw = 0, bool pool = false) {
   ConvArgs a{};
   a.out_hw = out_hw;
+  a.pool = pool;
   a.cus = c.cus;
   // Every other convolution of a partition walks its tiles backwards, so it
   // starts on the rows its producer wrote last, the ones most likely still in
@@ -608,11 +609,11 @@ hipError_t run_conv(const Ctx &c, const ConvSpec &cs, const void *x, const Act &
   }
   const double flops =
       2.0 * a.M * (double)a.N * (cs.s2d || cs.nhwc8 ? (double)cs.cin * cs.k * cs.k : (double)a.K);
-  const double bytes = (double)c.m.esz * ((double)nb * in.elems() + (double)a.M * a.N * (res ? 2 : 1) +
+  const double bytes = (double)c.m.esz * ((double)nb * in.elems() + (double)a.M * a.N * (res ? 2 : 1) / (pool ? 4 : 1) +
                                           (double)a.N * a.K + (cs.fused ? (double)a.M * cs.cin2 : 0.0));
   if (c.m.bf16)
     return timed(c.s, F_CONV_BF16, flops, bytes, [&] { return launch_conv_bf16(a, ld, c.s); });
-  if (out_hw) return hipErrorNotSupported;
+  if (out_hw || pool) return hipErrorNotSupported;
   a.splits = cs.splits;
   a.part = c.part;
   hipError_t r = timed(c.s, F_CONV_F32, flops, bytes, [&] { return launch_conv_f32(a, ld, c.s); });
@@ -634,15 +635,25 @@ bool stem_pool_fusable(const Model &m) {
   return stem_pool_supported(l0.in.c, l0.in.h, l0.in.w, cs.cout, l0.out.h, l0.out.w, l1.out.h, l1.out.w);
 }
 
-// Layer li (a convolution) and layer li + 1 (2 x 2 / 2 max pooling) that one
-// kernel runs: 3 x 3, stride 1, padding 1, 64 channels to 64, ReLU, bf16.
-bool pool_fusable(const Model &m, int li) {
+// Layer li, a bf16 convolution with ReLU over an NHWC activation, followed by
+// layer li + 1, 2 x 2 / 2 max pooling of its whole (even-sized) output: the
+// convolution's kernel can pool before it stores.
+bool pool_follows(const Model &m, int li) {
   if (!m.bf16 || li + 1 >= (int)m.layers.size()) return false;
   const LayerPlan &lp = m.layers[li], &pl = m.layers[li + 1];
   if (lp.L.kind != HAPI_CONV || !lp.L.relu || lp.convs.size() != 1) return false;
   const ConvSpec &cs = lp.convs[0];
   if (cs.s2d || cs.nhwc8 || cs.fused) return false;
   if (pl.L.kind != HAPI_MAXPOOL || pl.L.k != 2 || pl.L.stride != 2 || pl.L.pad != 0) return false;
+  return lp.out.h % 2 == 0 && lp.out.w % 2 == 0 && pl.out.h * 2 == lp.out.h && pl.out.w * 2 == lp.out.w;
+}
+
+// ... and the convolution is one the row-streaming 3 x 3 kernel runs (64
+// channels to 64, stride 1, padding 1), which pools in its own way.
+bool pool_fusable_c64(const Model &m, int li) {
+  if (!pool_follows(m, li)) return false;
+  const LayerPlan &lp = m.layers[li];
+  const ConvSpec &cs = lp.convs[0];
   return conv3x3_c64_supported(cs.cin, cs.cout, cs.k, cs.k, cs.stride, cs.pad, lp.in.w, cs.Kp, cs.cout, cs.cout) &&
          conv3x3_c64_pool_supported(lp.in.h, lp.in.w, cs.cout);
 }
@@ -743,11 +754,27 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
     const hapi_layer &L = lp.L;
     if (c.on_layer) c.on_layer(li, true);
     const bool nchw_in = (li == 0) && m.first_reads_nchw;
-    // A 3 x 3 convolution over 64 channels to 64 with ReLU followed by 2 x 2 / 2
-    // max pooling (VGG's conv1_2 + pool1), when its own output is not the
+    // A convolution with ReLU followed by 2 x 2 / 2 max pooling (VGG's
+    // conv1_2 + pool1 ... conv5_3 + pool5), when its own output is not the
     // split and layers are not being timed one by one: one kernel pools the
     // rounded result before storing it, bit for bit the two layers' output.
-    if (L.kind == HAPI_CONV && !nchw_in && !c.on_layer && li + 1 < split && pool_fusable(m, li)) {
+    // 64 channels to 64 at stride 1: the row-streaming 3 x 3 kernel; others:
+    // the implicit GEMM with its rows in pooling-window order, when the
+    // layer's kernel supports it (else the two layers run apart).
+    if (L.kind == HAPI_CONV && !nchw_in && !c.on_layer && li + 1 < split && !pool_fusable_c64(m, li) &&
+        pool_follows(m, li)) {
+      const int o = free_slot();
+      const hipError_t e = run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[o], nullptr, true, false, false, 0,
+                                    nullptr, nullptr, PreAct{}, 0, true);
+      if (e == hipSuccess) {
+        cur = c.slot[o];
+        cur_slot = o;
+        ++li;  // the pooling layer ran inside the convolution
+        continue;
+      }
+      if (e != hipErrorNotSupported) HIP_TRY(e);
+    }
+    if (L.kind == HAPI_CONV && !nchw_in && !c.on_layer && li + 1 < split && pool_fusable_c64(m, li)) {
       const ConvSpec &cs = lp.convs[0];
       const LayerPlan &pl = m.layers[li + 1];
       const int o = free_slot();

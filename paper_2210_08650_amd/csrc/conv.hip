@@ -745,10 +745,22 @@ struct WsPlan {
       const int m = m0 + (ga + i) * 8 + (lane >> 3);
       const int kc8 = ((ga + i) & 1) ? kcB : kcA;
       const bool valid = m < a.M;
-      const int hw = a.Ho * a.Wo;
       const int mm = valid ? m : 0;
-      const int n = mm / hw, rem = mm - n * hw;
-      const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
+      int n, ho, wo;
+      if (LD == LD_NHWC && a.pool) {  // row 4 window + 2 dy + dx
+        const int wp_n = a.Wo >> 1, hwp = (a.Ho >> 1) * wp_n;
+        const int win = mm >> 2;
+        n = win / hwp;
+        const int rem = win - n * hwp, hp = rem / wp_n;
+        ho = 2 * hp + ((mm >> 1) & 1);
+        wo = 2 * (rem - hp * wp_n) + (mm & 1);
+      } else {
+        const int hw = a.Ho * a.Wo;
+        n = mm / hw;
+        const int rem = mm - n * hw;
+        ho = rem / a.Wo;
+        wo = rem - ho * a.Wo;
+      }
       if (LD == LD_NHWC8) {
         // chunk kc8 / 8 of k-tile t is tap 8 t + kc8 / 8: the 8 channel slots
         // of one input pixel, or zeros (padding, taps past kh x kw)
@@ -1016,7 +1028,7 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   __syncthreads();
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
-  if (n >= a.N && !a.out_hw) return;
+  if (n >= a.N && !a.out_hw && !a.pool) return;
   float bias[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) bias[e] = (a.bias && n < a.N) ? a.bias[n + e] : 0.0f;
@@ -1046,13 +1058,33 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
       const float hi = epilogue_act(v[2 * e + 1], a.relu, a.gelu);
       o[e] = f2bf2(lo, hi);
     }
-    if (a.out_hw) {
+    if (a.out_hw || a.pool) {
       // the finished chunk back into the first half of its own staging
       // slot (no other thread reads that slot)
       *reinterpret_cast<uint4 *>(Cs + rr * SM::kCPitch + cc * 8) = make_uint4(o[0], o[1], o[2], o[3]);
     } else {
       *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
     }
+  }
+  if (a.pool) {
+    // 2 x 2 max pooling: staged rows 4 w .. 4 w + 3 are window w's pixels;
+    // their rounded, ReLU'd (non-negative) bf16 values compared as unsigned
+    // integers give the pooling layer's maximum.
+    __syncthreads();
+    const uint16_t *Cb = reinterpret_cast<const uint16_t *>(Cs);
+    for (int idx = t; idx < (BM / 4) * CPR; idx += NT) {
+      const int w = idx / CPR, c8 = idx - w * CPR;
+      const int m = m0 + 4 * w, nn = n0 + c8 * 8;
+      if (m >= a.M || nn >= a.N) continue;
+      uint4 v = *reinterpret_cast<const uint4 *>(Cb + (4 * w) * (2 * SM::kCPitch) + c8 * 16);
+#pragma unroll
+      for (int d = 1; d < 4; ++d) {
+        const uint4 u = *reinterpret_cast<const uint4 *>(Cb + (4 * w + d) * (2 * SM::kCPitch) + c8 * 16);
+        v = make_uint4(bf16x2_max(v.x, u.x), bf16x2_max(v.y, u.y), bf16x2_max(v.z, u.z), bf16x2_max(v.w, u.w));
+      }
+      *reinterpret_cast<uint4 *>(y + (int64_t)(m >> 2) * a.ldc + nn) = v;
+    }
+    return;
   }
   if (a.out_hw) {
     // NCHW store: consecutive threads take consecutive rows (pixels) of one
@@ -1086,6 +1118,7 @@ __global__ __launch_bounds__(2 * WM * WN * 64, 3) void conv_bf16_ws3_kernel(Conv
 
 template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 0, int MINB = 1, bool PRE = false>
 hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
+  if (a.pool && (EPI != 0 || LD != LD_NHWC)) return hipErrorNotSupported;  // pooling: staged epilogue
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if constexpr (MINB >= 3 && !PRE)
     hapi_launch((conv_bf16_ws3_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
@@ -1378,7 +1411,19 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
 #pragma unroll
               for (int e = 0; e < 4; ++e)
                 o[e] = f2bf2(epilogue_act(v[2 * e], a.relu, a.gelu), epilogue_act(v[2 * e + 1], a.relu, a.gelu));
-              if (m < a.M) *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+              if (a.pool) {
+                // 2 x 2 max pooling: rows 4 w .. 4 w + 3 (window w) are lanes
+                // l, l ^ 1, l ^ 2, l ^ 3; the window's first lane stores.
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  o[e] = bf16x2_max(o[e], (uint32_t)__shfl_xor((int)o[e], 1, 64));
+                  o[e] = bf16x2_max(o[e], (uint32_t)__shfl_xor((int)o[e], 2, 64));
+                }
+                if ((lrow & 3) == 0 && m < a.M)
+                  *reinterpret_cast<uint4 *>(y + (int64_t)(m >> 2) * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+              } else if (m < a.M) {
+                *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+              }
             }
           }
       }
@@ -1602,6 +1647,7 @@ hipError_t launch_pws_cfg(const ConvArgs &a, hipStream_t s) {
   const int cus = a.cus > 0 ? a.cus : cu_count();
   const int grid = tiles < cus ? tiles : cus;
   if (PRE && a.Kp > kPreMax) return hipErrorInvalidValue;
+  if (a.pool && (EP != 2 || LD != LD_NHWC)) return hipErrorNotSupported;  // pooling: 8-channel epilogue
   hapi_launch((conv_bf16_pws_kernel<BM, BN, WM, WN, PW, STAGES, LD, KW, EP, PRE>), dim3(grid),
                      dim3((WM * WN + PW) * 64), 0, s, a);
   return hipGetLastError();
@@ -1740,6 +1786,11 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
       return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
     } else if (a.K >= 2 * BK) {
       return launch_pws_ld<128, 256, 2, 4, 4, 3, LD, 2>(a, s);
+    }
+    // The pipelined kernels below do not pool.
+    if (a.pool) {
+      if (a.N <= 64) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+      return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
     }
   }
   if (a.N <= 64) {
@@ -1972,6 +2023,9 @@ hipError_t launch_f32_cfg(const ConvArgs &a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
+  if (a.pool && (ld != LD_NHWC || !a.relu || a.gelu || a.res || a.out_hw || a.pre_scale || a.lda || (a.Ho & 1) ||
+                 (a.Wo & 1) || a.N % 16 || a.ldc % 8 || !ws_eligible(a, ld)))
+    return hipErrorNotSupported;
   if (a.out_hw > 0 && ((ld != LD_GEMM && ld != LD_NHWC && ld != LD_CAT) || a.pre_scale || (a.lda && a.lda != a.K) ||
                        a.gelu || a.N % 8 || a.ldr % 8))
     return hipErrorNotSupported;
@@ -2000,7 +2054,7 @@ hipError_t launch_conv_bf16(const ConvArgs &a, Loader ld, hipStream_t s) {
     // The pipelined kernel needs 16-byte output rows; the register-staged one
     // handles element gathers (NCHW stems) and any other width.
     case LD_NHWC:
-      if (!a.gelu && !a.out_hw && a.Ho == a.H && a.Wo == a.W && conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
+      if (!a.gelu && !a.out_hw && !a.pool && a.Ho == a.H && a.Wo == a.W && conv3x3_c64_supported(a.C, a.N, a.kh, a.kw, a.stride, a.pad, a.W, a.Kp, a.ldc, a.ldr))
         return launch_conv3x3_c64(a.x, a.w, a.Kp, a.bias, a.res, a.ldr, a.y, a.ldc, a.n_img, a.H, a.W, a.relu != 0,
                                   a.cus > 0 ? a.cus : cu_count(), s);
       return (a.N % 8 == 0 && a.ldc % 8 == 0 && a.ldr % 8 == 0) ? launch_pipe_ld<LD_NHWC>(a, s)

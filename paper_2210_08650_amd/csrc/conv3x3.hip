@@ -269,9 +269,6 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
       // Max over the window (lanes l, l ^ 1, l ^ 16, l ^ 17) of the rounded,
       // non-negative bf16 values, compared as unsigned integers, as the
       // separate pooling layer computes it; the window's top-left lane stores.
-      auto pmax = [](uint32_t x, uint32_t y) -> uint32_t {
-        return max(x & 0xffffu, y & 0xffffu) | (max(x >> 16, y >> 16) << 16);
-      };
       if (ho < r1) {
         const bool store = (lrow & 0x11) == 0 && c0 + px < a.W;
         const int64_t pm = ((int64_t)img * (a.H / 2) + (row >> 1)) * (a.W / 2) + ((c0 + px) >> 1);
@@ -286,8 +283,8 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               o[e] = f2bf2(fmaxf(v[2 * e], 0.0f), fmaxf(v[2 * e + 1], 0.0f));
-              o[e] = pmax(o[e], (uint32_t)__shfl_xor((int)o[e], 1, 64));
-              o[e] = pmax(o[e], (uint32_t)__shfl_xor((int)o[e], 16, 64));
+              o[e] = bf16x2_max(o[e], (uint32_t)__shfl_xor((int)o[e], 1, 64));
+              o[e] = bf16x2_max(o[e], (uint32_t)__shfl_xor((int)o[e], 16, 64));
             }
             if (store) *reinterpret_cast<uint4 *>(y + pm * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
           }

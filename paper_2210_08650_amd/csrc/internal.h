@@ -21,6 +21,11 @@ __device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
   const f32x2_dev_t v = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_dev_t));
 }
+// Per-half maximum of two packed pairs of non-negative bf16 values: for those
+// the order of the bit patterns as unsigned integers is the order of the values.
+__device__ __forceinline__ uint32_t bf16x2_max(uint32_t x, uint32_t y) {
+  return max(x & 0xffffu, y & 0xffffu) | (max(x >> 16, y >> 16) << 16);
+}
 
 // ---------------------------------------------------------------- launches
 
@@ -105,6 +110,13 @@ struct ConvArgs {
   // launch_conv_bf16 returns hipErrorNotSupported when the layer's kernel
   // cannot store it, before launching anything.
   int out_hw;
+  // 1: the convolution is followed by 2 x 2 / 2 max pooling, which the
+  // epilogue applies before storing: GEMM row m is pixel
+  // (2 hp + (m & 2) / 2, 2 wp + (m & 1)) of pooling window m / 4 =
+  // (image, hp, wp), and y is the pooled output [M / 4][ldc].  bf16, NHWC
+  // loader, ReLU, even Ho and Wo, N % 16 == 0, no residual; launch_conv_bf16
+  // returns hipErrorNotSupported, having launched nothing, otherwise.
+  int pool;
   // fp32 only: the k-tiles split into `splits` consecutive slices computed by
   // separate workgroups into part [splits][M][N] (float32), then summed in
   // slice order (fixed, so results do not depend on M); splits <= 1: none.
