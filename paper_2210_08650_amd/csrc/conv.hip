@@ -435,6 +435,9 @@ struct PipeSmem {
 // swapped (weights as A, activations as B) so each lane's accumulators hold 4
 // consecutive output channels of one output pixel; the epilogue stores them
 // directly as 8-byte writes and the kernel needs no LDS beyond the stages.
+// EPI = 2 (warp-specialised kernel): operands swapped as for 1, a half-wave
+// exchange gives each lane 8 consecutive channels of its pixel, stored as one
+// 16-byte write; bias and residual are fetched before the k-loop.
 // ReLU(x * scale + shift) on 8 consecutive channels, rounded to bf16 once.
 __device__ __forceinline__ bf16x8_t preact8(bf16x8_t v, float4 s0, float4 s1, float4 h0, float4 h1) {
   typedef float f32x8_t __attribute__((ext_vector_type(8)));
@@ -814,6 +817,7 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[SM::kBytes];
   uint16_t *smem = reinterpret_cast<uint16_t *>(smem_raw);
   __shared__ __attribute__((aligned(16))) float pre_s[PRE ? 2 * kPreMax : 4];
+  __shared__ __attribute__((aligned(16))) float bias_s[EPI == 2 ? BN : 4];
 
   const int tiles_n = (a.N + BN - 1) / BN;
   const int tile = a.rev ? (int)gridDim.x - 1 - xcd_remap(blockIdx.x, gridDim.x) : xcd_remap(blockIdx.x, gridDim.x);
@@ -853,6 +857,31 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
       rpre[k] = (m < a.M && n < a.N) ? *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n)
                                       : make_uint4(0, 0, 0, 0);
     }
+  }
+  // EPI = 2: the tile's bias into LDS (written before this wave's first
+  // barrier, read after the last), and each consumer lane's residual chunks
+  // into registers: 8 channels at column 32 j + 16 p + 8 lh of row
+  // 32 i + lane % 32 of its block.
+  uint4 rdir[EPI == 2 ? TM : 1][EPI == 2 ? TN : 1][2];
+  if constexpr (EPI == 2) {
+    if (t < BN) bias_s[t] = (a.bias && n0 + t < a.N) ? a.bias[n0 + t] : 0.0f;
+    if (!producer && a.res) {
+      const uint16_t *res = static_cast<const uint16_t *>(a.res);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int p = 0; p < 2; ++p) {
+            const int m = m0 + wm * TM * 32 + 32 * i + lrow;
+            const int n = n0 + wn * TN * 32 + 32 * j + 16 * p + 8 * lh;
+            rdir[i][j][p] = (m < a.M && n < a.N) ? *reinterpret_cast<const uint4 *>(res + (int64_t)m * a.ldr + n)
+                                                 : make_uint4(0, 0, 0, 0);
+          }
+    }
+    // LDS writes done before the barrier that publishes them (lgkmcnt(0)
+    // only: the residual loads stay in flight)
+    __builtin_amdgcn_s_waitcnt(0xC07F);
   }
 
   if (producer) {
@@ -972,7 +1001,51 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
 
   uint16_t *y = static_cast<uint16_t *>(a.y);
   const uint16_t *res = static_cast<const uint16_t *>(a.res);
-  if (EPI) {
+  if constexpr (EPI == 2) {
+    if (producer) return;
+    // acc[i][j][4 g + e] = C[row 32 i + lane % 32][column 32 j + 8 g + 4 lh + e]
+    // of this wave's block; the lower half-wave keeps group 2 p and receives
+    // the upper half's, the upper half receives the lower half's group 2 p + 1.
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = m0 + wm * TM * 32 + 32 * i + lrow;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i][j][8 * p + e]),
+                                                              __float_as_uint(acc[i][j][8 * p + 4 + e]), false, false);
+            v[e] = __uint_as_float(sw2[0]);
+            v[4 + e] = __uint_as_float(sw2[1]);
+          }
+          const int c = wn * TN * 32 + 32 * j + 16 * p + 8 * lh, n = n0 + c;
+          if (n >= a.N) continue;
+          const float4 b0 = *reinterpret_cast<const float4 *>(bias_s + c);
+          const float4 b1 = *reinterpret_cast<const float4 *>(bias_s + c + 4);
+          v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+          v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+          if (res) {
+            const uint4 rv = rdir[i][j][p];
+            const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] += bf2f((uint16_t)(w4[e] & 0xffff));
+              v[2 * e + 1] += bf2f((uint16_t)(w4[e] >> 16));
+            }
+          }
+          uint32_t o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            o[e] = f2bf2(epilogue_act(v[2 * e], a.relu, a.gelu), epilogue_act(v[2 * e + 1], a.relu, a.gelu));
+          if (m < a.M) *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+    }
+    return;
+  }
+  if (EPI == 1) {
     if (producer) return;
     // acc[i][j][4g + e] = C[m][n + e], m = block row + lane % 32,
     // n = block column + 8 g + 4 (lane / 32).
@@ -1118,6 +1191,9 @@ __global__ __launch_bounds__(2 * WM * WN * 64, 3) void conv_bf16_ws3_kernel(Conv
 
 template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 0, int MINB = 1, bool PRE = false>
 hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
+  // the NCHW split store and pooling need the staged epilogue
+  if constexpr (EPI == 2)
+    if (a.out_hw || a.pool) return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, KW, 0, MINB, PRE>(a, s);
   if (a.pool && (EPI != 0 || LD != LD_NHWC)) return hipErrorNotSupported;  // pooling: staged epilogue
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if constexpr (MINB >= 3 && !PRE)
@@ -1731,7 +1807,7 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
   if (LD == LD_GEMM && a.Kp == BK && a.N <= 64 && !a.res) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s);
   if (LD == LD_GEMM && a.Kp == 2 * BK && a.N == 512 && a.res) return launch_short_ld<128, 64, 2, 2, LD, 3>(a, s);
   if (ws_eligible(a, (Loader)LD)) {
-    if (LD == LD_S2D) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+    if (LD == LD_S2D) return launch_ws_ld<128, 64, 2, 2, 3, LD, 2, 2>(a, s);
     // With one partition in flight (none other fills the CUs this launch
     // leaves idle):
     // - fewer 128 x 128 tiles than half the CUs: 64 x 64 tiles, four stages
@@ -1744,7 +1820,7 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     //   with two partitions in flight the larger tiles win throughout
     //   (ResNet-50 b256: 70.1k against 67.2k img/s).
     if (a.lanes <= 1 && a.N >= 64 && 2 * (int64_t)((a.M + 127) / 128) * ((a.N + 127) / 128) < a.cus)
-      return launch_ws_ld<64, 64, 2, 2, 4, LD, 0, 2>(a, s);
+      return launch_ws_ld<64, 64, 2, 2, 4, LD, 2, 2>(a, s);
     if (a.lanes <= 1 && a.N >= 128 && a.K >= 1024 &&
         2 * (int64_t)((a.M + 255) / 256) * ((a.N + 127) / 128) < a.cus)
       return launch_pws_ld<128, 128, 2, 2, 4, 4, LD, 2>(a, s);
@@ -1752,13 +1828,13 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     // works on padding; 32 x 32 per consumer wave, three stages (DenseNet-121
     // b256: 56.8k -> 57.7k img/s against 256 x 32 tiles for large M and
     // 128 x 64 tiles, half of them padding, for small M).
-    if (a.N <= 32 && a.K >= 2 * BK) return launch_ws_ld<128, 32, 4, 1, 3, LD, 0, 2>(a, s);
+    if (a.N <= 32 && a.K >= 2 * BK) return launch_ws_ld<128, 32, 4, 1, 3, LD, 2, 2>(a, s);
     if (a.N <= 64) {
-      if (a.K >= 512 || a.K == BK) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
+      if (a.K >= 512 || a.K == BK) return launch_ws_ld<128, 64, 2, 2, 3, LD, 2, 2>(a, s);
     } else if (a.res) {
       if (a.K >= 2 * BK) {
-        if (a.N >= 1024) return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
-        return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+        if (a.N >= 1024) return launch_ws_ld<128, 64, 2, 2, 2, LD, 2, 3>(a, s);
+        return launch_ws_ld<128, 128, 2, 2, 2, LD, 2, 2>(a, s);
       }
     } else if (LD == LD_CAT) {
       if (a.N <= 128) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
@@ -1773,9 +1849,9 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
       // the latency-bound three-workgroups-per-CU tiles
       if (a.kh == 1 && a.K >= 512) {
         if (a.lanes >= 2) return launch_pws_ld<256, 128, 4, 2, 4, 3, LD, 2>(a, s);
-        return launch_ws_ld<128, 64, 2, 2, 2, LD, 0, 3>(a, s);
+        return launch_ws_ld<128, 64, 2, 2, 2, LD, 2, 3>(a, s);
       }
-      if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+      if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 2, 2>(a, s);
     } else if (a.N >= 512 && a.K >= 2048) {
       // The longest reductions with enough rows, partitions in flight:
       // 128 x 256 tiles (VGG-16 b128 conv4/conv5 and ResNet-50 b256 stage-4
@@ -1789,8 +1865,8 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     }
     // The pipelined kernels below do not pool.
     if (a.pool) {
-      if (a.N <= 64) return launch_ws_ld<128, 64, 2, 2, 3, LD, 0, 2>(a, s);
-      return launch_ws_ld<128, 128, 2, 2, 2, LD, 0, 2>(a, s);
+      if (a.N <= 64) return launch_ws_ld<128, 64, 2, 2, 3, LD, 2, 2>(a, s);
+      return launch_ws_ld<128, 128, 2, 2, 2, LD, 2, 2>(a, s);
     }
   }
   if (a.N <= 64) {
