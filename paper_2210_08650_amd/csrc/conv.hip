@@ -525,6 +525,14 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
                                       : make_uint4(0, 0, 0, 0);
     }
   }
+  // The staged epilogue's bias (8 channels per thread), loaded here for the
+  // same reason: read after the k-loop, its latency would fall in the epilogue.
+  float bpre[EPI ? 1 : 8];
+  if constexpr (!EPI) {
+    const int n = n0 + (t % CPR) * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bpre[e] = (a.bias && n < a.N) ? a.bias[n + e] : 0.0f;
+  }
 
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
@@ -652,9 +660,7 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
   if (n >= a.N && !a.out_hw) return;
-  float bias[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) bias[e] = (a.bias && n < a.N) ? a.bias[n + e] : 0.0f;
+  const float *bias = bpre;
   uint16_t *y = static_cast<uint16_t *>(a.y);
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
