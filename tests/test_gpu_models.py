@@ -92,6 +92,33 @@ def _vit_small(depth=2):
             OM.vit(image=64, patch=16, dim=128, heads=2, mlp=256, depth=depth, name="vit_small"))
 
 
+@pytest.mark.parametrize("image", [112, 176, 192, 240])
+def test_attention_token_counts_match_oracle(image):
+    """The attention kernel at token counts whose padded width differs from
+    ViT-B/16's 224 (50, 122, 145 and 226 tokens: 64, 128, 160 and 256), with
+    fewer (image, head) pairs than CUs.  The attention branch is isolated as
+    in test_vit_sub_layer_branches (MLP output projection zeroed, attention
+    projection scaled up) so that the block's change of the residual stream
+    is the attention output alone."""
+    layers = PM.vit(image=image, patch=16, dim=128, heads=2, mlp=256, depth=1)
+    om = OM.vit(image=image, patch=16, dim=128, heads=2, mlp=256, depth=1, name=f"vit_{image}")
+    ps = synth.params(62, om.manifest())
+    base = 4  # after patch weight, bias, class token, position embedding
+    for i in (base + 10, base + 11):
+        ps[i] = np.zeros_like(ps[i])
+    for i in (base + 4, base + 5):
+        ps[i] = (ps[i] * 16.0).astype(np.float32)
+    shape = (3, image, image)
+    r = Runner(layers, H.HAPI_BF16, ps, shape)
+    xd, xv = images_for(H.HAPI_BF16, synth.images(63, 2, *shape))
+    outs = om.forward(ps, xv, om.n_layers - 1, collect=True)
+    d_ref = outs[3] - outs[2]
+    d_got = r.extract_np(xd, 3) - r.extract_np(xd, 2)
+    err = rel_l2(d_got, d_ref)
+    print(f"attention, {outs[3].shape[1]} tokens: rel_l2 {err:.3e}", flush=True)
+    assert err <= 2e-2
+
+
 @pytest.mark.parametrize("branch", ["attention", "mlp"])
 def test_vit_sub_layer_branches(branch):
     # Isolate one branch: zero the other branch's output projection and scale
