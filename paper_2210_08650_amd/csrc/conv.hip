@@ -1858,6 +1858,11 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
         return launch_ws_ld<128, 64, 2, 2, 2, LD, 2, 3>(a, s);
       }
       if (a.K >= 2 * BK) return launch_ws_ld<128, 128, 2, 2, 2, LD, 2, 2>(a, s);
+    } else if (LD == LD_GEMM && a.N >= 2048 && a.K <= 1024) {
+      // Wide linear layers with a short reduction (ViT qkv and fc1):
+      // warp-specialised 128 x 128 tiles (ViT-B/16 qkv at 64 images 56.8 us
+      // against 58-65 us with persistent 128 x 256 tiles).
+      return launch_ws_ld<128, 128, 2, 2, 2, LD, 2, 2>(a, s);
     } else if (a.N >= 512 && a.K >= 2048) {
       // The longest reductions with enough rows, partitions in flight:
       // 128 x 256 tiles (VGG-16 b128 conv4/conv5 and ResNet-50 b256 stage-4
