@@ -258,18 +258,17 @@ __global__ __launch_bounds__(kThreads) void conv_bf16_kernel(ConvArgs a) {
 //
 // For inputs whose 8-element k-chunks are contiguous 16-byte runs (NHWC with
 // C % 64 == 0, row-major matrices, NCHW patches) the tiles are moved by
-// global_load_lds_dwordx4: each lane's 16 bytes land directly in LDS, so no
-// registers or ds_write instructions are spent on staging and STAGES - 1
-// k-tiles are in flight while the MFMAs consume the oldest one.  Padding taps
-// and rows beyond M / N read a zero chunk in global memory instead.
+// buffer_load ... lds (16 bytes per lane): each lane's 16 bytes land directly
+// in LDS, so no registers or ds_write instructions are spent on staging and
+// STAGES - 1 k-tiles are in flight while the MFMAs consume the oldest one.
+// Padding taps and rows beyond M / N use a byte offset outside the buffer's
+// range, which reads zeros.
 //
 // LDS rows hold 64 bf16 (128 B) without padding; the 16-byte chunk kc of row
 // r is stored at position kc ^ ((r >> 1) & 7).  The LDS serves 256 bytes (64
 // banks) per clock, i.e. two 128-byte rows: with this swizzle the 16 rows a
 // quarter-wave fragment read touches land in 16 distinct 16-byte slots of
 // that 256-byte window, so fragment reads are free of bank conflicts.
-
-__device__ __attribute__((aligned(64))) uint4 g_zero_chunk[4];
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
@@ -280,12 +279,23 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+constexpr unsigned kOob = 0x80000000u;  // a byte offset outside every buffer range
+
+// Moves 16 bytes per lane from base + soff + voff (a raw buffer of 2^31 - 1
+// bytes: offsets at or beyond kOob read zeros) into LDS at lds + 16 * lane.
+// Only scalar instructions besides the load itself.
+__device__ __forceinline__ void dma16(const void *base, uint16_t *lds, unsigned voff, unsigned soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7fffffff, 0x00020000), LDS_PTR(lds), 16,
+      voff, soff, 0, 0);
+}
+
 // Addressing of the LDS DMA that moves one k-tile (64 k values) of the
 // implicit-GEMM operands: A rows (output pixels, gathered through the loader
 // LD) and B rows (packed weights [N][Kp]).  One DMA instruction moves 8 rows of
 // 8 16-byte chunks; this thread's instructions are A row-groups ga0 .. ga0+NA-1
-// and B row-groups gb0 .. gb0+NB-1.  Rows beyond M / N and padding taps read
-// the zero chunk in global memory instead, so the address arithmetic stays
+// and B row-groups gb0 .. gb0+NB-1.  Rows beyond M / N and padding taps get
+// an out-of-range offset (zeros), so the address arithmetic stays
 // branch-free.
 //
 // Lane l of row-group g fills row 8 g + l / 8, physical chunk l % 8, i.e.
@@ -337,7 +347,6 @@ struct DmaPlan {
   // stage whose A and B parts start at As and Bs.
   __device__ __forceinline__ void issue(const ConvArgs &a, int kt, uint16_t *As, uint16_t *Bs, int q0,
                                         int q1) const {
-    const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero_chunk);
     const uint16_t *x = static_cast<const uint16_t *>(a.x);
     const uint16_t *wp = static_cast<const uint16_t *>(a.w);
     const int kbase = kt * BK;
@@ -382,14 +391,14 @@ struct DmaPlan {
         ok = rhi[i] > -(1 << 27) && k0 < a.K;
         off = roff[i] + (c * a.H + rhi[i] + u) * a.W + rwi[i] + vv;
       }
-      const uint16_t *src = ok ? xs + off : zero;
-      __builtin_amdgcn_global_load_lds(src, LDS_PTR(As + (ga0 + i) * 512), 16, 0, 0);
+      // 32-bit byte offsets (the launcher checks every operand fits in
+      // 2^31 bytes); a chunk outside the image or past K reads zeros
+      dma16(xs, As + (ga0 + i) * 512, ok ? (unsigned)off * 2u : kOob, 0);
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       if (NA + j < q0 || NA + j >= q1) continue;
-      const uint16_t *src = bok[j] ? wp + boffs[j] + kbase : zero;
-      __builtin_amdgcn_global_load_lds(src, LDS_PTR(Bs + (gb0 + j) * 512), 16, 0, 0);
+      dma16(wp, Bs + (gb0 + j) * 512, bok[j] ? (unsigned)(boffs[j] + kbase) * 2u : kOob, 0);
     }
   }
 };
@@ -724,17 +733,6 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_bf16_pipe_kernel(ConvArgs a
 // buffer's scalar offset).  One s_barrier per k-tile, reached by all waves,
 // hands a landed stage to the consumers and a consumed stage back to the
 // producers.
-constexpr unsigned kOob = 0x80000000u;  // a byte offset outside every buffer range
-
-// Moves 16 bytes per lane from base + soff + voff (a raw buffer of 2^31 - 1
-// bytes: offsets at or beyond kOob read zeros) into LDS at lds + 16 * lane.
-// Only scalar instructions besides the load itself.
-__device__ __forceinline__ void dma16(const void *base, uint16_t *lds, unsigned voff, unsigned soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7fffffff, 0x00020000), LDS_PTR(lds), 16,
-      voff, soff, 0, 0);
-}
-
 // Per-lane offsets of one producer lane.  Row-group g = ga + i (A) or gb + j
 // (B) covers rows 8 g .. 8 g + 7; lane l moves row 8 g + l / 8 and logical
 // chunk (l % 8) ^ ((row >> 1) & 7) of the 64-wide k-tile, as in DmaPlan.
@@ -1221,8 +1219,27 @@ hipError_t launch_bf16_cfg(const ConvArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Whether every element offset the pipelined kernel's DMA forms stays below
+// 2^30 (byte offsets below 2^31).
+template <int LD>
+bool pipe_offsets_fit(const ConvArgs &a) {
+  const int64_t lim = (int64_t)1 << 30;
+  if ((int64_t)a.N * a.Kp >= lim) return false;
+  if (LD == LD_GEMM) return (int64_t)a.M * (a.lda ? a.lda : a.K) < lim;
+  if (LD == LD_CAT && (int64_t)a.n_img * a.H2 * a.W2 * a.C2 >= lim) return false;
+  return (int64_t)a.n_img * a.C * a.H * a.W < lim;
+}
+
 template <int BM, int BN, int WM, int WN, int STAGES, int LD, int SCHED = 1, int EPI = 0, bool PRE = false>
 hipError_t launch_pipe_cfg(const ConvArgs &a, hipStream_t s) {
+  // The DMA addresses every operand with 32-bit byte offsets: past 2^31 bytes
+  // the register-staged kernel (64-bit addresses) takes the element-gather
+  // loaders, and the others report the size as unsupported.
+  if (!pipe_offsets_fit<LD>(a)) {
+    if constexpr (!PRE && (LD == LD_GEMM || LD == LD_NHWC || LD == LD_NCHW_PATCH))
+      return launch_bf16_cfg<BM, BN, LD>(a, s);
+    return hipErrorInvalidValue;
+  }
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   hapi_launch((conv_bf16_pipe_kernel<BM, BN, WM, WN, STAGES, LD, SCHED, EPI, PRE>), dim3(tiles),
                      dim3(WM * WN * 64), 0, s, a);
