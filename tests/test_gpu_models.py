@@ -228,6 +228,42 @@ def test_profile_time_matches_extraction(batch, chunk, inflight):
     assert lo <= ratio <= hi
 
 
+def test_profile_vgg16_times_every_boundary():
+    """VGG-16's profile times all its layer boundaries (each pooling runs as a
+    layer of its own there, although extraction fuses it into the preceding
+    convolution), and the per-layer times add up to within [0.8, 2.0] of an
+    extraction to the last boundary at the same batch."""
+    batch, split = 32, 18
+    d = H.Desc(PM.vgg16(), H.HAPI_BF16, stream=torch.cuda.current_stream())
+    need = H.hapi_workspace_bytes(d, batch, split, True)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    d.set(workspace=ws, workspace_bytes=need)
+    b, us = H.hapi_profile_layers(d, batch, True)
+    assert us[0] == 0.0 and all(t > 0 for t in us[1:split + 1]), us
+    assert b == H.hapi_profile_layers(d, batch)[0]
+    prof_ms = sum(us[1:split + 1]) / 1e3
+    r, _, _, xd, _, _ = _setup("vgg16", 74, batch)
+    r.extract(xd, split)  # warm
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ts = []
+    need = H.hapi_workspace_bytes(r.desc.set(chunk=0, inflight=0), batch, split)
+    w2 = torch.empty(need, dtype=torch.uint8, device="cuda")
+    out = torch.empty((batch,) + tuple(r.out_shape(split)), dtype=torch.bfloat16, device="cuda")
+    r.desc.set(workspace=w2, workspace_bytes=need)
+    for _ in range(5):
+        torch.cuda.synchronize()
+        ev[0].record()
+        H.hapi_extract(r.desc, r.packed, xd, batch, split, out)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ts.append(ev[0].elapsed_time(ev[1]))
+    ext_ms = sorted(ts)[len(ts) // 2]
+    ratio = prof_ms / ext_ms
+    print(f"vgg16 profile b{batch}: {split} boundaries, sum {prof_ms:.3f} ms, extraction {ext_ms:.3f} ms, "
+          f"ratio {ratio:.2f}", flush=True)
+    assert 0.8 <= ratio <= 2.0
+
+
 def test_kernel_stats_count_launches():
     r, _, _, xd, _, _ = _setup("resnet50", 72, 2)
     H.hapi_stats_enable(True)
