@@ -1044,7 +1044,19 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             o[e] = f2bf2(epilogue_act(v[2 * e], a.relu, a.gelu), epilogue_act(v[2 * e + 1], a.relu, a.gelu));
-          if (m < a.M) *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+          if (a.pool) {
+            // 2 x 2 max pooling: rows 4 w .. 4 w + 3 (window w) are lanes
+            // l, l ^ 1, l ^ 2, l ^ 3; the window's first lane stores.
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              o[e] = bf16x2_max(o[e], (uint32_t)__shfl_xor((int)o[e], 1, 64));
+              o[e] = bf16x2_max(o[e], (uint32_t)__shfl_xor((int)o[e], 2, 64));
+            }
+            if ((lrow & 3) == 0 && m < a.M)
+              *reinterpret_cast<uint4 *>(y + (int64_t)(m >> 2) * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+          } else if (m < a.M) {
+            *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
+          }
         }
     }
     return;
@@ -1195,10 +1207,10 @@ __global__ __launch_bounds__(2 * WM * WN * 64, 3) void conv_bf16_ws3_kernel(Conv
 
 template <int BM, int BN, int WM, int WN, int STAGES, int LD, int KW, int EPI = 0, int MINB = 1, bool PRE = false>
 hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
-  // the NCHW split store and pooling need the staged epilogue
+  // the NCHW split store needs the staged epilogue
   if constexpr (EPI == 2)
-    if (a.out_hw || a.pool) return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, KW, 0, MINB, PRE>(a, s);
-  if (a.pool && (EPI != 0 || LD != LD_NHWC)) return hipErrorNotSupported;  // pooling: staged epilogue
+    if (a.out_hw) return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, KW, 0, MINB, PRE>(a, s);
+  if (a.pool && (EPI == 1 || LD != LD_NHWC)) return hipErrorNotSupported;  // pooling: EPI 0 or 2
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if constexpr (MINB >= 3 && !PRE)
     hapi_launch((conv_bf16_ws3_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
