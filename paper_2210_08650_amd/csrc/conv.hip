@@ -1117,7 +1117,7 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   __syncthreads();
   const int cc = t % CPR;
   const int n = n0 + cc * 8;
-  if (n >= a.N && !a.out_hw && !a.pool) return;
+  if (n >= a.N && !a.out_hw) return;
   float bias[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) bias[e] = (a.bias && n < a.N) ? a.bias[n + e] : 0.0f;
@@ -1147,33 +1147,13 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
       const float hi = epilogue_act(v[2 * e + 1], a.relu, a.gelu);
       o[e] = f2bf2(lo, hi);
     }
-    if (a.out_hw || a.pool) {
+    if (a.out_hw) {
       // the finished chunk back into the first half of its own staging
       // slot (no other thread reads that slot)
       *reinterpret_cast<uint4 *>(Cs + rr * SM::kCPitch + cc * 8) = make_uint4(o[0], o[1], o[2], o[3]);
     } else {
       *reinterpret_cast<uint4 *>(y + (int64_t)m * a.ldc + n) = make_uint4(o[0], o[1], o[2], o[3]);
     }
-  }
-  if (a.pool) {
-    // 2 x 2 max pooling: staged rows 4 w .. 4 w + 3 are window w's pixels;
-    // their rounded, ReLU'd (non-negative) bf16 values compared as unsigned
-    // integers give the pooling layer's maximum.
-    __syncthreads();
-    const uint16_t *Cb = reinterpret_cast<const uint16_t *>(Cs);
-    for (int idx = t; idx < (BM / 4) * CPR; idx += NT) {
-      const int w = idx / CPR, c8 = idx - w * CPR;
-      const int m = m0 + 4 * w, nn = n0 + c8 * 8;
-      if (m >= a.M || nn >= a.N) continue;
-      uint4 v = *reinterpret_cast<const uint4 *>(Cb + (4 * w) * (2 * SM::kCPitch) + c8 * 16);
-#pragma unroll
-      for (int d = 1; d < 4; ++d) {
-        const uint4 u = *reinterpret_cast<const uint4 *>(Cb + (4 * w + d) * (2 * SM::kCPitch) + c8 * 16);
-        v = make_uint4(bf16x2_max(v.x, u.x), bf16x2_max(v.y, u.y), bf16x2_max(v.z, u.z), bf16x2_max(v.w, u.w));
-      }
-      *reinterpret_cast<uint4 *>(y + (int64_t)(m >> 2) * a.ldc + nn) = v;
-    }
-    return;
   }
   if (a.out_hw) {
     // NCHW store: consecutive threads take consecutive rows (pixels) of one
@@ -1210,7 +1190,7 @@ hipError_t launch_ws_cfg(const ConvArgs &a, hipStream_t s) {
   // the NCHW split store needs the staged epilogue
   if constexpr (EPI == 2)
     if (a.out_hw) return launch_ws_cfg<BM, BN, WM, WN, STAGES, LD, KW, 0, MINB, PRE>(a, s);
-  if (a.pool && (EPI == 1 || LD != LD_NHWC)) return hipErrorNotSupported;  // pooling: EPI 0 or 2
+  if (a.pool && (EPI != 2 || LD != LD_NHWC)) return hipErrorNotSupported;  // pooling: register epilogue
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if constexpr (MINB >= 3 && !PRE)
     hapi_launch((conv_bf16_ws3_kernel<BM, BN, WM, WN, STAGES, LD, KW, EPI>), dim3(tiles),
