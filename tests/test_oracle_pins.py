@@ -498,3 +498,30 @@ def test_densenet121_vs_torch_functional():
 def test_dense_block_net_shapes():
     m = M.dense_block_net()
     assert m.shapes() == [(3, 224, 224), (64, 112, 112), (64, 56, 56), (192, 56, 56)]
+
+
+# Total learnable parameters of the TorchVision models the paper uses (as
+# TorchVision documents them for alexnet, vgg16, resnet18, resnet50,
+# densenet121 and vit_b_16), and the size of the classifier head each adds
+# after the feature extractor the oracle assembles (closed forms).
+TORCHVISION_TOTALS = {
+    "alexnet": (61_100_840, (9216 * 4096 + 4096) + (4096 * 4096 + 4096) + (4096 * 1000 + 1000)),
+    "vgg16": (138_357_544, (25088 * 4096 + 4096) + (4096 * 4096 + 4096) + (4096 * 1000 + 1000)),
+    "resnet18": (11_689_512, 512 * 1000 + 1000),
+    "resnet50": (25_557_032, 2048 * 1000 + 1000),
+    "densenet121": (7_978_856, 1024 * 1000 + 1000),
+    "vit_b16": (86_567_656, 768 * 1000 + 1000),
+}
+
+
+@pytest.mark.parametrize("name", sorted(TORCHVISION_TOTALS))
+def test_feature_extractor_parameter_counts(name):
+    """Structural pin: the oracle's learnable parameters (weights, biases,
+    batch-norm and layer-norm scale and shift, class token, position
+    embedding; not the batch-norm running statistics) number exactly the
+    TorchVision model's total less its classifier head.  A misread width,
+    kernel size, block count or a missing normalisation changes the count."""
+    total, head = TORCHVISION_TOTALS[name]
+    m = M.build(name)
+    n = sum(int(np.prod(shape)) for shape, kind in m.manifest() if kind not in ("bn_mean", "bn_var"))
+    assert n == total - head, (name, n, total - head)
