@@ -17,7 +17,7 @@ OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhapi.so")
 ARCH = os.environ.get("HAPI_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["conv.hip", "conv3x3.hip", "conv_first.hip", "stem.hip", "attention.hip", "elementwise.hip",
+SOURCES = ["conv.hip", "conv3x3.hip", "conv_first.hip", "stem.hip", "attention.hip", "elementwise.hip", "bottleneck.hip",
            "api.cpp", "split.cpp"]
 HEADERS = [os.path.join(CSRC, "internal.h"), os.path.join(ROOT, "include", "hapi.h")]
 

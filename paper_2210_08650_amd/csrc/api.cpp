@@ -679,6 +679,23 @@ bool expand_fusable(const LayerPlan &lp) {
          conv3x3_c64_expand_supported(c3.cout, c3.K, c3.Kp, c3.cout, c3.cout);
 }
 
+// Layer li, a bf16 bottleneck with an identity shortcut and a plain expanding
+// 1 x 1 convolution, followed by layer li + 1, a bottleneck whose first
+// convolution reduces li's output with a 1 x 1: the two 1 x 1 convolutions
+// run as one kernel (bottleneck_link_supported's shapes).
+bool link_fusable(const Model &m, int li) {
+  if (!m.bf16 || li + 1 >= (int)m.layers.size()) return false;
+  const LayerPlan &lp = m.layers[li], &ln = m.layers[li + 1];
+  if (lp.L.kind != HAPI_BOTTLENECK || lp.has_sc || lp.convs.size() != 3 || lp.convs[2].fused) return false;
+  if (ln.L.kind != HAPI_BOTTLENECK || ln.convs.empty()) return false;
+  if (expand_fusable(lp)) return false;
+  const ConvSpec &c3 = lp.convs[2], &c1 = ln.convs[0];
+  if (c3.k != 1 || c3.stride != 1 || c3.pad != 0 || c1.k != 1 || c1.stride != 1 || c1.pad != 0) return false;
+  if (c1.cin != c3.cout || lp.out.h != ln.in.h || lp.out.w != ln.in.w || lp.in.h != lp.out.h || lp.in.w != lp.out.w)
+    return false;
+  return bottleneck_link_supported(c3.cin, c3.cout, c1.cout, c3.Kp, c1.Kp);
+}
+
 // Runs layers start+1..split on nb images of `images` (the layer-`start`
 // tensor in the caller layout); writes the split output (caller layout) to
 // `out` unless it is null (profiling).
@@ -732,6 +749,7 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
     return HAPI_OK;
   };
   int li0 = start;
+  int linked = -1;  // slot holding the next bottleneck's first convolution, when already run
   // Stem convolution and max pooling in one kernel when the stem output is
   // not itself the split and layers are not being timed one by one.
   if (start == 0 && split >= 2 && !c.on_layer && stem_pool_fusable(m) && (uintptr_t)images % 4 == 0) {
@@ -869,11 +887,14 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
         break;
       }
       case HAPI_BOTTLENECK: {
-        const int A = free_slot(), B = free_slot(A);
+        // The previous block's kernel already ran this block's first
+        // convolution into slot `linked`.
+        const int A = linked >= 0 ? linked : free_slot(), B = free_slot(A);
         const int width = L.width;
         const Act a1{width, lp.in.h, lp.in.w, false};
         const Act a2{width, lp.out.h, lp.out.w, false};
-        HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
+        if (linked < 0) HIP_TRY(run_conv(c, lp.convs[0], cur, lp.in, nb, c.slot[A], nullptr, true, false, false));
+        linked = -1;
         if (expand_fusable(lp)) {
           // The 3 x 3 and the expanding 1 x 1 in one kernel, in place over the
           // block input (each output element's residual is read by the lane
@@ -892,6 +913,25 @@ int run_chunk(const Ctx &c, const void *images, int nb, int start, int split, vo
           break;
         }
         HIP_TRY(run_conv(c, lp.convs[1], c.slot[A], a1, nb, c.slot[B], nullptr, true, false, false));
+        if (!c.on_layer && li + 1 < split && link_fusable(m, li)) {
+          // This block's expansion (in place over the block input, which is
+          // its residual) and the next block's reduction (into slot A, free
+          // once the 3 x 3 has read it) in one kernel.
+          const ConvSpec &c3 = lp.convs[2], &n1 = m.layers[li + 1].convs[0];
+          const double px = (double)nb * a2.h * a2.w;
+          const double flops = 2.0 * px * ((double)c3.cout * c3.K + (double)n1.cout * n1.K);
+          const double bytes = (double)m.esz * (px * (c3.cin + 2.0 * c3.cout + n1.cout) + (double)c3.cout * c3.Kp +
+                                                (double)n1.cout * n1.Kp);
+          HIP_TRY(timed(c.s, F_CONV_BF16, flops, bytes, [&] {
+            return launch_bottleneck_link(c.slot[B], c.pk + c3.pk_w, reinterpret_cast<const float *>(c.pk + c3.pk_b),
+                                          cur, c.slot[cur_slot], c.pk + n1.pk_w,
+                                          reinterpret_cast<const float *>(c.pk + n1.pk_b), c.slot[A],
+                                          nb * a2.h * a2.w, c3.cin, c3.cout, n1.cout, c.s);
+          }));
+          cur = c.slot[cur_slot];
+          linked = A;
+          break;
+        }
         if (lp.convs[2].fused) {  // c3 and the projection shortcut in one GEMM, into the free slot
           if (int r = last_conv(li, lp.convs[2], c.slot[B], a2, A, nullptr, true, cur, &lp.in)) return r;
           cur = c.slot[A];

@@ -203,6 +203,16 @@ bool conv_first_supported(const ConvArgs &a);
 hipError_t launch_conv_first(const ConvArgs &a, hipStream_t s);
 // Compute units of the current device.
 int cu_count();
+// Two consecutive bottlenecks joined at their boundary: block i's expanding
+// 1 x 1 convolution (b3 [M][ci] -> y [M][e], bias3, residual res [M][e],
+// ReLU; y may equal res) and block i + 1's reducing 1 x 1 convolution
+// (y -> a1 [M][co], bias1, ReLU) in one kernel, bit for bit the two
+// convolutions.  w3 [e][ci] and w1 [co][e] packed bf16 (Kp == K).  Shapes
+// outside bottleneck_link_supported: hipErrorInvalidValue, nothing launched.
+bool bottleneck_link_supported(int ci, int e, int co, int kp3, int kp1);
+hipError_t launch_bottleneck_link(const void *b3, const void *w3, const float *bias3, const void *res, void *y,
+                                  const void *w1, const float *bias1, void *a1, int M, int ci, int e, int co,
+                                  hipStream_t s);
 bool stem_pool_supported(int C, int H, int W, int cout, int Ho, int Wo, int Hp, int Wp);
 hipError_t launch_stem_pool_bf16(const void *x, const void *w, int ldw, const float *bias, void *y, int n, int C,
                                  int H, int W, int Ho, int Wo, int Hp, int Wp, int cus, hipStream_t s);

@@ -45,6 +45,11 @@ hipError_t launch_conv3x3_c64(const void *, const void *, int, const float *, co
 bool conv3x3_c64_pool_supported(int, int, int) { return false; }
 bool conv3x3_c64_expand_supported(int, int, int, int, int) { return false; }
 bool conv_first_supported(const ConvArgs &) { return false; }
+bool bottleneck_link_supported(int, int, int, int, int) { return false; }
+hipError_t launch_bottleneck_link(const void *, const void *, const float *, const void *, void *, const void *,
+                                  const float *, void *, int, int, int, int, hipStream_t) {
+  return none();
+}
 hipError_t launch_conv_first(const ConvArgs &, hipStream_t) { return none(); }
 int cu_count() { return 256; }
 bool stem_pool_supported(int, int, int, int, int, int, int, int) { return false; }

@@ -567,3 +567,43 @@ def test_conv_pool_fused_is_bit_exact(shape, cout, batch, passes):
     print(f"conv+pool {shape}->{cout} b{batch}: {tuple(a.shape)}, separate pooling passes {pools}", flush=True)
     assert pools == passes
     assert torch.equal(a, b)
+
+
+# (input shape, batch): ResNet-50 stage-2 blocks on 28 x 28 (M = 2352 ... 50176
+# rows, several waves of 64-row workgroups) and on a 10 x 13 map (ragged last
+# row tile).
+LINK_CASES = [((512, 28, 28), 3), ((512, 10, 13), 3), ((512, 28, 28), 64), ((512, 7, 9), 1)]
+
+
+@pytest.mark.parametrize("shape,batch", LINK_CASES)
+def test_bottleneck_link_is_bit_exact(shape, batch):
+    """Between two bottlenecks (identity shortcut, then a 1x1 reduction) the
+    first block's expansion and the next block's reduction run as one kernel;
+    it must equal, bit for bit, the blocks run apart (an identity pooling in
+    between keeps them apart), for a reduction to 128 (stage 2 -> stage 2) and
+    to 256 (stage 2 -> stage 3, whose 3x3 has stride 2)."""
+    c = shape[0]
+    blocks = [OM.Bottleneck(c, 128, 1), OM.Bottleneck(512, 128, 1), OM.Bottleneck(512, 256, 2)]
+    om = OM.Model("link", [OM.MaxPool(1, 1)] + blocks, shape)
+    ps = synth.params(24, om.manifest())
+    b = [dict(kind=H.HAPI_BOTTLENECK, cin=c, width=128, cout=512, stride=1),
+         dict(kind=H.HAPI_BOTTLENECK, cin=512, width=128, cout=512, stride=1),
+         dict(kind=H.HAPI_BOTTLENECK, cin=512, width=256, cout=1024, stride=2)]
+    ident = PM.maxpool(1, 1)
+    linked = Runner([ident] + b, H.HAPI_BF16, ps, shape)
+    apart = Runner([ident, b[0], ident, b[1], ident, b[2]], H.HAPI_BF16, ps, shape)
+    xd, _ = images_for(H.HAPI_BF16, synth.images(25, batch, *shape))
+    launches = []
+    for r, split in ((linked, 4), (apart, 6)):
+        H.hapi_stats_enable(True)
+        r.extract(xd, split)
+        st = {s["name"]: s for s in H.hapi_stats_collect()}
+        H.hapi_stats_enable(False)
+        launches.append(st["conv_bf16"]["launches"])
+    for k in (2, 3, 4):  # every block boundary: outputs of blocks 1, 2, 3
+        a = linked.extract(xd, k)
+        e = apart.extract(xd, 2 * k - 2)
+        print(f"link {shape} b{batch} block {k - 1}: {tuple(a.shape)}", flush=True)
+        assert torch.equal(a, e), k
+    print(f"link {shape} b{batch}: conv launches linked {launches[0]}, apart {launches[1]}", flush=True)
+    assert launches[1] - launches[0] == 2
