@@ -26,7 +26,7 @@ import numpy as np
 
 PEAK = {"bf16": 2500.0, "f32": 157.3}  # dense MFMA TFLOP/s (MI355X)
 # Sources of the convolution kernel family whose counters the traffic profile holds.
-CONV_SOURCES = ("conv.hip", "conv3x3.hip", "stem.hip")
+CONV_SOURCES = ("conv.hip", "conv3x3.hip", "stem.hip", "bottleneck.hip")
 HBM_PEAK = 8000.0                      # GB/s
 
 
