@@ -109,20 +109,24 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
   // Input row h (-1 .. H) lives in ring slot (h + 1) % kRing; outside the
   // image and in the padding columns it is zero.  Item it moves 16 bytes.
   // Branch-free: a chunk outside the image reads the image's first pixel and
-  // is zeroed when stored, so the loads of a whole row set stay in flight.
+  // is zeroed (a select) only when stored, so the loads of a whole row set
+  // stay in flight; zeroing a load's destination right after issuing it
+  // would make the wave wait for that load first.
+  auto row_ok = [&](int h, int it) {
+    const int col = c0 + (it >> 3) - 1;  // ring pixel p holds column c0 + p - 1
+    return it < kRowChunks && (unsigned)h < (unsigned)a.H && (unsigned)col < (unsigned)a.W;
+  };
   auto load_row = [&](int h, int it) -> uint4 {
-    const int p = it >> 3, c = it & 7;  // ring pixel p holds column c0 + p - 1
-    const int col = c0 + p - 1;
-    const bool ok = it < kRowChunks && (unsigned)h < (unsigned)a.H && (unsigned)col < (unsigned)a.W;
-    const int64_t pix = ok ? (int64_t)h * a.W + col : 0;
-    uint4 v = *reinterpret_cast<const uint4 *>(a.x + ((img_px + pix) << 6) + c * 8);
-    if (!ok) v = make_uint4(0u, 0u, 0u, 0u);
-    return v;
+    const int p = it >> 3, c = it & 7;
+    const int64_t pix = row_ok(h, it) ? (int64_t)h * a.W + c0 + p - 1 : 0;
+    return *reinterpret_cast<const uint4 *>(a.x + ((img_px + pix) << 6) + c * 8);
   };
   constexpr int kPer = (kRowChunks + kThreads - 1) / kThreads;  // chunks per thread per row
   auto store_row = [&](int h, int it, const uint4 &v) {
     const int p = it >> 3, c = it & 7;
-    *reinterpret_cast<uint4 *>(ring + ring_off((h + 1) % kRing, p, c)) = v;
+    const uint32_t keep = row_ok(h, it) ? ~0u : 0u;
+    *reinterpret_cast<uint4 *>(ring + ring_off((h + 1) % kRing, p, c)) =
+        make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep);
   };
 
   // Prologue: every load (weights and the first six input rows) is issued
@@ -198,18 +202,21 @@ __global__ __launch_bounds__(kThreads, 1) void conv3x3_c64_kernel(Conv3Args a) {
     const bool live = row < r1 && c0 + px < a.W;
     // EXPAND: the residual of this lane's outputs, loaded now so that its
     // latency hides behind the 3 x 3 MFMAs.  Part (h, jn, q) holds channels
-    // 128 h + 32 jn + 16 q + 8 lh .. + 8 of pixel px.
+    // 128 h + 32 jn + 16 q + 8 lh .. + 8 of pixel px.  The loads are
+    // unconditional (a lane outside the band reads its image's first pixel;
+    // its outputs are never stored): a register zeroed for some lanes before
+    // its load is issued makes the wave wait for every load in flight,
+    // the next rows' included.
     uint4 rr[EXPAND ? 2 : 1][EXPAND ? 4 : 1][2];
     if constexpr (EXPAND) {
+      const int64_t mr = live ? m : img_px;
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int jn = 0; jn < 4; ++jn)
 #pragma unroll
           for (int q = 0; q < 2; ++q)
-            rr[h][jn][q] = (live && a.res)
-                               ? *reinterpret_cast<const uint4 *>(a.res + m * a.ldr + 128 * h + 32 * jn + 16 * q + 8 * lh)
-                               : make_uint4(0u, 0u, 0u, 0u);
+            rr[h][jn][q] = *reinterpret_cast<const uint4 *>(a.res + mr * a.ldr + 128 * h + 32 * jn + 16 * q + 8 * lh);
     }
     f32x16_t acc[2];
 #pragma unroll
@@ -409,6 +416,7 @@ hipError_t launch_conv3x3_c64(const void *x, const void *w, int ldw, const float
                               void *y, int ldc, int n, int H, int W, bool relu, int cus, hipStream_t s,
                               const void *w3, int ldw3, const float *bias3, bool pool) {
   if (pool && (w3 || res || !relu || !conv3x3_c64_pool_supported(H, W, ldc))) return hipErrorInvalidValue;
+  if (w3 && !res) return hipErrorInvalidValue;
   // Enough workgroups to fill the CUs: split images into strips of columns,
   // then into bands of rows.
   const int strips = (W + kPix - 3) / (kPix - 2);

@@ -78,25 +78,34 @@ __global__ __launch_bounds__(64 * kFirstWaves) void conv_first_kernel(ConvArgs a
 
   // B fragments of the 32 output pixels from column wo0: the 8 slots of the
   // input pixel under this lane's tap, zero outside the image.  Branch-free:
-  // a chunk outside reads the image's first pixel and is zeroed.
-  auto load = [&](int wo0, bf16x8_t xf[KS]) {
+  // a chunk outside reads the image's first pixel; bit s of the mask says
+  // whether k-step s is inside, and the zeroing (a select) happens where the
+  // fragment is used: zeroing a load's destination right after issuing it
+  // would make the wave wait for that load first.
+  auto load = [&](int wo0, bf16x8_t xf[KS], uint32_t &okm) {
     const int wo = wo0 + lrow;
     const int wi0 = wo * a.stride - a.pad;
+    okm = 0;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int hi = hi0 + du[s], wi = wi0 + dv[s];
       const bool ok = tap_ok[s] && wo < a.Wo && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
       const int64_t pix = ok ? img_px + (int64_t)hi * a.W + wi : img_px;
-      uint4 v = *reinterpret_cast<const uint4 *>(x + pix * 8);
-      if (!ok) v = make_uint4(0u, 0u, 0u, 0u);
-      xf[s] = __builtin_bit_cast(bf16x8_t, v);
+      xf[s] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4 *>(x + pix * 8));
+      okm |= ok ? 1u << s : 0u;
     }
+  };
+  auto masked = [](bf16x8_t f, uint32_t okm, int s) {
+    const uint32_t keep = (okm >> s) & 1u ? ~0u : 0u;
+    const uint4 v = __builtin_bit_cast(uint4, f);
+    return __builtin_bit_cast(bf16x8_t, make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep));
   };
 
   bf16x8_t cur[KS], nxt[KS];
-  load(0, cur);
+  uint32_t okc, okn = 0;
+  load(0, cur, okc);
   for (int wo0 = 0; wo0 < a.Wo; wo0 += 32) {
-    if (wo0 + 32 < a.Wo) load(wo0 + 32, nxt);  // next block's loads fly over this block's MFMAs and stores
+    if (wo0 + 32 < a.Wo) load(wo0 + 32, nxt, okn);  // next block's loads fly over this block's MFMAs and stores
     f32x16_t acc[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j)
@@ -104,8 +113,9 @@ __global__ __launch_bounds__(64 * kFirstWaves) void conv_first_kernel(ConvArgs a
       for (int e = 0; e < 16; ++e) acc[j][e] = 0.0f;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[0][s], cur[s], acc[0], 0, 0, 0);
-      acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[1][s], cur[s], acc[1], 0, 0, 0);
+      const bf16x8_t b = masked(cur[s], okc, s);
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[0][s], b, acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[1][s], b, acc[1], 0, 0, 0);
     }
     // acc[j][4 g + e] = channel 32 j + 8 g + 4 (lane / 32) + e of pixel wo0 + lane % 32;
     // after the exchange of part q a lane owns channels 32 j + 16 q + 8 (lane / 32) .. + 8.
@@ -145,6 +155,7 @@ __global__ __launch_bounds__(64 * kFirstWaves) void conv_first_kernel(ConvArgs a
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int s = 0; s < KS; ++s) cur[s] = nxt[s];
+    okc = okn;
   }
 }
 

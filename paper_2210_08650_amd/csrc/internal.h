@@ -186,8 +186,9 @@ constexpr int kS2DChannels = 16;
 bool conv3x3_c64_supported(int C, int N, int kh, int kw, int stride, int pad, int W, int Kp, int ldc, int ldr);
 // With w3 (packed [256][ldw3], K = 64) the ReLU'd, bf16-rounded result is
 // expanded in the same kernel by a 1 x 1 convolution to 256 channels with
-// bias3, the residual res [.][ldr] and ReLU, into y [.][ldc] (a bottleneck's
-// last two convolutions); see conv3x3_c64_expand_supported.
+// bias3, the residual res [.][ldr] (required: hipErrorInvalidValue without)
+// and ReLU, into y [.][ldc] (a bottleneck's last two convolutions); see
+// conv3x3_c64_expand_supported.
 // pool: the ReLU'd result goes through 2 x 2 / 2 max pooling first, y being
 // the pooled output [n, H/2, W/2][ldc] (relu, no residual, no expansion;
 // see conv3x3_c64_pool_supported).
