@@ -49,21 +49,28 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attention_kernel(const uin
   const bool stager = t < 2 * TP;
   const int kb = t >> 3, sc = t & 7;
   uint4 kv[4], vv[4];
+  // Keys past T read key T - 1 and are zeroed when stored (a select): a
+  // register zeroed before its load is issued makes the wave wait for every
+  // load in flight first.
   auto stage_load = [&](int pair) {
+    if (!stager) return;
     const int img = pair / heads, h = pair - img * heads;
     const uint16_t *base = qkv + (int64_t)img * T * ld;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int s = 4 * kb + r;
-      kv[r] = vv[r] = make_uint4(0, 0, 0, 0);
-      if (stager && s < T) {
-        kv[r] = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + D + h * DH + sc * 8);
-        vv[r] = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + 2 * D + h * DH + sc * 8);
-      }
+      const int s = min(4 * kb + r, T - 1);
+      kv[r] = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + D + h * DH + sc * 8);
+      vv[r] = *reinterpret_cast<const uint4 *>(base + (int64_t)s * ld + 2 * D + h * DH + sc * 8);
     }
   };
   auto stage_store = [&](int buf) {
     if (!stager) return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t keep = 4 * kb + r < T ? ~0u : 0u;
+      kv[r] = make_uint4(kv[r].x & keep, kv[r].y & keep, kv[r].z & keep, kv[r].w & keep);
+      vv[r] = make_uint4(vv[r].x & keep, vv[r].y & keep, vv[r].z & keep, vv[r].w & keep);
+    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) *reinterpret_cast<uint4 *>(Ks[buf] + (4 * kb + r) * KP + sc * 8) = kv[r];
     auto half = [&](const uint4 &q, int e) -> uint32_t {
@@ -82,18 +89,15 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attention_kernel(const uin
   const int q = wave * 32 + col;
   const bool qblock = wave * 32 < T;
   bf16x8_t qf[DH / 16];
+  // Query rows past T read query T - 1: their scores and outputs stay in
+  // their own rows, which are never stored.
   auto load_q = [&](int pair) {
     const int img = pair / heads, h = pair - img * heads;
     const uint16_t *base = qkv + (int64_t)img * T * ld;
+    const int qr = min(q, T - 1);
 #pragma unroll
-    for (int ks = 0; ks < DH / 16; ++ks) {
-      if (q < T) {
-        qf[ks] = *reinterpret_cast<const bf16x8_t *>(base + (int64_t)q * ld + h * DH + ks * 16 + hl * 8);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qf[ks][e] = (__bf16)0.0f;
-      }
-    }
+    for (int ks = 0; ks < DH / 16; ++ks)
+      qf[ks] = *reinterpret_cast<const bf16x8_t *>(base + (int64_t)qr * ld + h * DH + ks * 16 + hl * 8);
   };
 
   int p = blockIdx.x;
