@@ -1415,6 +1415,11 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
   // 32 j + 16 part + 8 lh (part 0..1).  Row 32 i + lane % 32 of the block.
   constexpr int NPART = EP == 2 ? 2 : 4;
   using ResT = typename std::conditional<EP == 2, uint4, uint2>::type;
+  // The tile loop is instantiated twice, reading the bias from LDS or (N
+  // beyond the LDS copy) from global memory, so that no epilogue wait
+  // covers the other path's counter.
+  auto consume = [&](auto lds_bias) {
+  constexpr bool kLdsBias = decltype(lds_bias)::value;
   int q = 0;
   for (int ti = t_lo; ti < t_hi; ++ti) {
     const int tile = a.rev ? t_lo + t_hi - 1 - ti : ti;
@@ -1482,13 +1487,19 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
             }
             const int n = nw + 32 * j + 16 * p + 8 * lh;
             if (n < a.N) {
-              if (bias_lds || a.bias) {
-                const float *bsrc = bias_lds ? bias_s + n : a.bias + n;
-                const float4 b0 = *reinterpret_cast<const float4 *>(bsrc);
-                const float4 b1 = *reinterpret_cast<const float4 *>(bsrc + 4);
-                v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
-                v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+              // LDS or global memory, never one pointer to either: that
+              // would be a flat load, which waits for every store of the
+              // wave still in flight.
+              float4 b0 = make_float4(0.f, 0.f, 0.f, 0.f), b1 = b0;
+              if constexpr (kLdsBias) {
+                b0 = *reinterpret_cast<const float4 *>(bias_s + n);
+                b1 = *reinterpret_cast<const float4 *>(bias_s + n + 4);
+              } else if (a.bias) {
+                b0 = *reinterpret_cast<const float4 *>(a.bias + n);
+                b1 = *reinterpret_cast<const float4 *>(a.bias + n + 4);
               }
+              v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+              v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
               if (res) {
                 const uint4 rv = rr[i][j][p];
                 const uint32_t w4[4] = {rv.x, rv.y, rv.z, rv.w};
@@ -1527,10 +1538,11 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int col = 32 * j + 8 * g + 4 * lh, n = nw + col;
-            const float4 bv = n >= a.N ? make_float4(0.f, 0.f, 0.f, 0.f)
-                              : bias_lds ? *reinterpret_cast<const float4 *>(bias_s + n)
-                              : a.bias   ? *reinterpret_cast<const float4 *>(a.bias + n)
-                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+            float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);  // LDS or global, never a flat load
+            if (n < a.N) {
+              if constexpr (kLdsBias) bv = *reinterpret_cast<const float4 *>(bias_s + n);
+              else if (a.bias) bv = *reinterpret_cast<const float4 *>(a.bias + n);
+            }
             float v[4] = {acc[i][j][4 * g] + bv.x, acc[i][j][4 * g + 1] + bv.y, acc[i][j][4 * g + 2] + bv.z,
                           acc[i][j][4 * g + 3] + bv.w};
             if (res) {
@@ -1567,6 +1579,9 @@ __global__ __launch_bounds__((WM * WN + PW) * 64, 1) void conv_bf16_pws_kernel(C
       }
     }
   }
+  };
+  if (bias_lds) consume(std::true_type{});
+  else consume(std::false_type{});
 }
 
 // ------------------------------------- bf16, short-K (one or two k-tiles)
