@@ -1007,6 +1007,11 @@ __device__ __forceinline__ void conv_bf16_ws_body(const ConvArgs &a) {
   const uint16_t *res = static_cast<const uint16_t *>(a.res);
   if constexpr (EPI == 2) {
     if (producer) return;
+    // The residual loads, issued before the k-loop, have landed long ago:
+    // one explicit wait here tells the compiler so, and spares every later
+    // part the wait it would otherwise place behind the earlier parts'
+    // stores (loads and stores share the vector-memory counter).
+    wait_vmcnt<0>();
     // acc[i][j][4 g + e] = C[row 32 i + lane % 32][column 32 j + 8 g + 4 lh + e]
     // of this wave's block; the lower half-wave keeps group 2 p and receives
     // the upper half's, the upper half receives the lower half's group 2 p + 1.
