@@ -1854,6 +1854,13 @@ hipError_t launch_pipe_ld(const ConvArgs &a, hipStream_t s) {
     //   M = 12544: 196 tiles) 256 x 128 stays faster, 60 against 73 us, and
     //   with two partitions in flight the larger tiles win throughout
     //   (ResNet-50 b256: 70.1k against 67.2k img/s).
+    // - 3 x 3 reductions of K >= 2048 with at most half as many 64 x 64 tiles
+    //   as CUs: 32 x 64 tiles, four stages, so twice the CUs walk the long
+    //   k-chain (ResNet-50 b8 stage-3 3 x 3 11.3 -> 10.3 us, stage 4
+    //   18.9 -> 16.7 us; with more tiles, as at b32, 64 x 64 stays faster);
+    if (a.lanes <= 1 && a.kh == 3 && a.K >= 2048 && a.N >= 64 &&
+        2 * (int64_t)((a.M + 63) / 64) * ((a.N + 63) / 64) <= a.cus)
+      return launch_ws_ld<32, 64, 1, 2, 4, LD, 2, 2>(a, s);
     if (a.lanes <= 1 && a.N >= 64 && 2 * (int64_t)((a.M + 127) / 128) * ((a.N + 127) / 128) < a.cus)
       return launch_ws_ld<64, 64, 2, 2, 4, LD, 2, 2>(a, s);
     if (a.lanes <= 1 && a.N >= 128 && a.K >= 1024 &&
