@@ -68,6 +68,9 @@ BF16_CASES = [
     (True, 128, 32, 3, 1, 1, 15, 3),     # 32 output channels, few rows: 128 x 32 tiles, ragged M
     (True, 128, 32, 3, 1, 1, 256, 2),    # 32 output channels, M = 131072: 128 x 32 tiles
     (True, 128, 24, 3, 1, 1, 256, 2),    # 24 output channels in a 32-column tile
+    (True, 256, 256, 3, 1, 1, 7, 3),     # K = 2304, few rows: 32 x 64 tiles, ragged M
+    (True, 512, 512, 3, 1, 1, 7, 2),     # K = 4608 (72 k-tiles) on 32 x 64 tiles
+    (True, 256, 256, 3, 1, 1, 14, 16),   # K = 2304, more rows: 64 x 64 tiles, four stages
 ]
 
 
