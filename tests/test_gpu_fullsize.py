@@ -69,11 +69,11 @@ def test_resnet50_batch_512_two_full_partitions():
     assert np.array_equal(r.extract_np(xd[:256].contiguous(), 18), got[:256])
 
 
-@pytest.mark.parametrize("batch", [8, 32, 128])
+@pytest.mark.parametrize("batch", [8, 16, 32, 128])
 def test_resnet50_sweep_sampled(batch):
     """The rest of the ResNet-50 batch sweep, each batch in the benchmark's
     launch configuration (automatic partitions; tile choice depends on the
-    rows of each layer and on the partitions in flight: one at 8 and 32, two
+    rows of each layer and on the partitions in flight: one at 8, 16 and 32, two
     64-image partitions at 128), against the oracle on images 0, B/2 and B-1.
     Storage-side batch adaptation must not change the result, so image 0 also
     equals its value in a batch of 256 bit for bit."""
